@@ -1,0 +1,237 @@
+#!/usr/bin/env python3
+"""Benchmark of the benchmarking-command hot path on one MI355X.
+
+A step is one whole large-GEMM benchmarking command (the gemm_large
+workload): generate A and B (bf16 4096 x 4096, normal(0, 1), Philox seed 1),
+compute the candidate C (bf16) and the fp32 reference C with the library
+GEMM as stand-ins for an agent's kernel and reference, check C against the
+reference (rtol 1.6e-2, atol 1e-2), then time the candidate in a critical
+region: 10 warm-up launches and 200 timed reps, each preceded by a 1 GiB
+cache flush (Section 2.1; Section 4.1; Section 4.2 step 5).
+
+Metric: generate + check + flush GB/s = algorithmic bytes of those kernels
+(bytes written by generation and flush, bytes read by the check) divided by
+their summed device time, measured with HIP events on the stream they run
+on. The roofline object is for the dominant kernel (the flush: 200 GiB of
+the step's 200.2 GiB). The timed-region inflation half of the metric is
+measured by `--fidelity` (Section 6.3, Eq. 1), which prints its own line.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+       python bench.py --fidelity [--samples S]
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+import uuid
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+GIB = 1 << 30
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def _sha256(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def _traffic_for(kernel_key):
+    """HBM bytes per launch from the committed rocprofv3 PMC summary, or None
+    when it is missing or the kernel source changed since it was taken."""
+    path = os.path.join(PROFILES, "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        data = json.load(f)
+    ent = data.get(kernel_key)
+    src = os.path.join(ROOT, "paper_2609_30057_amd", "csrc", "kernels.hip")
+    if not ent or ent.get("kernels_hip_sha256") != _sha256(src):
+        return None
+    return ent.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(step_bytes):
+    """The oracle (single-threaded C) on a bounded sample of one step: both
+    generated matrices and the full check, plus 20 of the 200 1 GiB flushes
+    (host fill of a pre-touched buffer), scaled to one step's byte mix."""
+    import numpy as np
+    import oracle
+    from paper_2609_30057_amd import workloads as W
+    cfg = W.GEMM_LARGE
+    n2 = cfg["n"] * cfg["n"]
+    offA, offB = W.gemm_large_offsets()
+    t0 = time.perf_counter()
+    A = oracle.gen("bf16", n2, cfg["seed"], offA, 1, 0.0, 1.0)
+    B = oracle.gen("bf16", n2, cfg["seed"], offB, 1, 0.0, 1.0)
+    t_gen = time.perf_counter() - t0
+    cref = oracle.gen("f32", n2, 77, 0, 1, 0.0, 1.0)      # reference-shaped fp32 operand
+    t0 = time.perf_counter()
+    oracle.check(A, "bf16", cref, "f32", cfg["rtol"], cfg["atol"])
+    t_check = time.perf_counter() - t0
+    buf = np.zeros(GIB // 4, dtype=np.uint32)
+    oracle.flush_fill(buf, 1)                              # first touch, not timed
+    sample_flushes = 20
+    t0 = time.perf_counter()
+    for r in range(sample_flushes):
+        oracle.flush_fill(buf, (0x9E3779B9 * (r + 1)) & 0xFFFFFFFF)
+    t_flush = (time.perf_counter() - t0) * (cfg["reps"] / sample_flushes)
+    total = t_gen + t_check + t_flush
+    del buf
+    return {
+        "value": round(step_bytes / total / 1e9, 3),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": ("one gemm_large step on the host: generation of both 4096x4096 bf16 normal matrices "
+                   "(%.2f s), the full 16.8M-element bf16-vs-fp32 check (%.2f s), and 20 of the 200 1 GiB "
+                   "flush fills scaled x10 (%.2f s); single-threaded C oracle" % (t_gen, t_check, t_flush)),
+    }
+
+
+def run_gemm_large(steps, warmup, with_cpu):
+    import numpy as np
+    import torch
+
+    import paper_2609_30057_amd as krex
+    from paper_2609_30057_amd import workloads as W
+
+    cfg = W.GEMM_LARGE
+    n = cfg["n"]
+    n2 = n * n
+    offA, offB = W.gemm_large_offsets()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    A = torch.empty(n, n, dtype=torch.bfloat16, device=dev)
+    B = torch.empty_like(A)
+    C = torch.empty_like(A)
+    Cl = torch.empty_like(A)
+    Af = torch.empty(n, n, dtype=torch.float32, device=dev)
+    Bf = torch.empty_like(Af)
+    Cref = torch.empty_like(Af)
+    fl = torch.empty(cfg["flush_bytes"] // 4, dtype=torch.int32, device=dev)
+    res = krex.check_result_buffer(dev)
+    shm = "/krex-bench-%s" % uuid.uuid4().hex[:10]
+    krex.attach(0, shm_name=shm)
+
+    gen_bytes = 2 * n2 * 2
+    check_bytes = n2 * (2 + 4)
+    flush_bytes = cfg["reps"] * cfg["flush_bytes"]
+    step_bytes = gen_bytes + check_bytes + flush_bytes
+
+    def candidate():
+        torch.matmul(A, B, out=Cl)
+
+    def one_step():
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+        ev[0].record()
+        krex.gen(A, cfg["seed"], offA, "normal", 0.0, 1.0)
+        ev[1].record()
+        krex.gen(B, cfg["seed"], offB, "normal", 0.0, 1.0)
+        ev[2].record()
+        torch.matmul(A, B, out=C)
+        Af.copy_(A)
+        Bf.copy_(B)
+        torch.matmul(Af, Bf, out=Cref)
+        ev[3].record()
+        krex.check(C.view(-1), Cref.view(-1), cfg["rtol"], cfg["atol"], out=res, sync=False)
+        ev[4].record()
+        times, ftimes = krex.time_loop(candidate, cfg["warmup"], cfg["reps"], flush_buf=fl, region=True,
+                                       with_flush_times=True)
+        verdict = krex.decode_check_result(res)
+        return dict(gen_ms=[ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2])],
+                    check_ms=ev[3].elapsed_time(ev[4]), flush_ms=ftimes, loop_ms=times, verdict=verdict)
+
+    for _ in range(warmup):
+        one_step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    recs = [one_step() for _ in range(steps)]
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    krex.detach()
+
+    gen_ms = np.array([sum(r["gen_ms"]) for r in recs])
+    check_ms = np.array([r["check_ms"] for r in recs])
+    flush_ms = np.array([f for r in recs for f in r["flush_ms"]])
+    kernel_s = (gen_ms.sum() + check_ms.sum() + flush_ms.sum()) / 1e3
+    value = steps * step_bytes / kernel_s / 1e9
+    flush_gbps = cfg["flush_bytes"] / (flush_ms.mean() / 1e3) / 1e9
+    traffic = _traffic_for("k_flush/gemm_large")
+    v = recs[-1]["verdict"]
+    out = {
+        "metric": "gen+check+flush GB/s vs MI355X HBM peak; p95 in-region timing inflation",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": round(wall / steps * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": ("gemm_large: A,B bf16 4096x4096 normal(0,1) Philox seed 1 (B at offset 16777216); "
+                         "bf16 candidate C vs fp32 reference C checked at rtol 1.6e-2 atol 1e-2; "
+                         "10 warm-up + 200 timed reps of the candidate in a critical region, 1 GiB flush "
+                         "before each rep"),
+            "elements_per_matrix": n2,
+            "flush_bytes": cfg["flush_bytes"],
+            "reps": cfg["reps"],
+            "algorithmic_bytes_per_step": step_bytes,
+        },
+        "roofline": {
+            "kernel": "k_flush",
+            "bound": "hbm",
+            "achieved": round(flush_gbps, 1),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(flush_gbps / HBM_PEAK_GBPS, 4),
+            "traffic": traffic,
+        },
+        "per_kernel": {
+            "gen_bf16_normal": {"ms": round(float(gen_ms.mean() / 2), 4),
+                                "GBps": round(n2 * 2 / (gen_ms.mean() / 2 / 1e3) / 1e9, 1)},
+            "check_bf16_f32": {"ms": round(float(check_ms.mean()), 4),
+                               "GBps": round(check_bytes / (check_ms.mean() / 1e3) / 1e9, 1)},
+            "flush_1GiB": {"ms": round(float(flush_ms.mean()), 4), "GBps": round(flush_gbps, 1)},
+        },
+        "wall_GBps": round(steps * step_bytes / wall / 1e9, 2),
+        "candidate_median_ms": round(float(np.median(recs[-1]["loop_ms"])), 4),
+        "verdict": {"mismatches": v.mismatches, "nan_count": v.nan_count, "max_abs": v.max_abs,
+                    "argmax_abs": v.argmax_abs, "max_rel": v.max_rel},
+    }
+    if with_cpu:
+        out["cpu_baseline"] = cpu_baseline(step_bytes)
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--fidelity", action="store_true")
+    ap.add_argument("--samples", type=int, default=300)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (use --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    if args.fidelity:
+        from paper_2609_30057_amd import fidelity
+        print(json.dumps(fidelity.run(samples=args.samples)), flush=True)
+        return
+    out = run_gemm_large(args.steps, args.warmup, not args.no_cpu_baseline)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,247 @@
+/*
+ * krex.h -- C ABI of the MI355X (gfx950) hot path of a kernel benchmarking
+ * command: seeded input generation, mismatch injection, the allclose
+ * correctness check, the cache flush, and the timed loop inside a critical
+ * region that excludes sibling processes sharing the GPU.
+ *
+ * Paper: KREX, "Concurrent Kernel Benchmarking on Shared GPUs via
+ * Region-Granular Exclusivity". A benchmarking command generates inputs,
+ * checks the candidate against a reference and then times it (Section 1;
+ * Section 2.1). Generation and checking produce values, not timings, and
+ * must give the same tensors and verdict under contention (Section 2.1,
+ * "Benchmarking command"). Only the timed loop needs the device to itself;
+ * it is marked as a critical region (Section 3, R1; Section 4.1), entered by
+ * lock -> gate -> drain -> cache flush and left by wait -> reopen -> unlock
+ * (Section 4.2, steps 1-3, 5, 6, 8), with the AMD variant's completion
+ * counters (Section 5).
+ *
+ * Conventions for every entry point:
+ *  - Status: KREX_OK (0) on success, a positive value for success with a
+ *    note, a negative KREX_E* code on failure. No exception crosses the ABI.
+ *    Argument errors are detected before anything is launched, so
+ *    KREX_EINVAL / KREX_EALIGN have no side effects.
+ *  - Memory: the caller owns every buffer. Pointers named "device" must be
+ *    device memory of the current HIP device (hipMalloc, or torch CUDA
+ *    tensors on ROCm). The library never allocates or frees them.
+ *  - Streams: `stream` is a hipStream_t passed as void* (NULL = the legacy
+ *    default stream). Kernel entry points are stream-ordered and return once
+ *    the work is enqueued.
+ *  - Gating: after krex_attach (gate on), every enqueueing entry point
+ *    follows counter-and-gate (Section 4.2, "GPU exclusivity"): it counts
+ *    itself in flight, then checks the region gate; if another process
+ *    holds a region it retracts, parks (spin, then futex) until the gate
+ *    reopens, and retries. The count is released when the device finishes
+ *    the work (Section 5, AMD), or at once when the launch fails (Section
+ *    4.2: the counter is decremented on error returns too). Without
+ *    krex_attach the kernel entry points run ungated.
+ *  - Failures are explicit (Section 4.3: unsupported calls fail rather than
+ *    bypass): a HIP error returns KREX_EHIP and krex_last_hip_error() gives
+ *    the hipError_t of the calling thread.
+ */
+#ifndef KREX_H
+#define KREX_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t krex_status;
+
+#define KREX_OK 0
+#define KREX_RECOVERED 1        /* region lock taken over from a dead holder */
+#define KREX_EINVAL (-1)        /* bad argument value */
+#define KREX_EALIGN (-2)        /* pointer not aligned to its element size */
+#define KREX_EHIP (-3)          /* HIP runtime error, see krex_last_hip_error */
+#define KREX_ETIMEDOUT (-4)     /* region entry or gate wait timed out */
+#define KREX_ESTATE (-5)        /* call not valid in this state (nesting, ...) */
+#define KREX_ENOTATTACHED (-6)  /* region call without krex_attach */
+#define KREX_ENOMEM (-7)        /* host allocation failed */
+#define KREX_EPEER (-8)         /* shared segment unusable (version, peer died in init) */
+#define KREX_ESYS (-9)          /* POSIX call failed (shm, futex, threads) */
+
+/* Element types. KREX_F8E4M3 is OCP fp8 e4m3fn (bias 7, max 448, no
+ * infinity), gfx950's native fp8. KREX_U32 is the raw 32-bit word stream. */
+#define KREX_F32 0
+#define KREX_BF16 1
+#define KREX_F16 2
+#define KREX_F8E4M3 3
+#define KREX_U32 4
+
+/* Value distributions of krex_gen. */
+#define KREX_UNIFORM 0   /* [p0, p1): u = (W >> 8) 2^-24, v = p0 + (p1 - p0) u */
+#define KREX_NORMAL 1    /* mean p0, std p1: Box-Muller on word pairs */
+#define KREX_BITCAST 2   /* the word's bits read as an fp32 value (any pattern) */
+
+/* Injection modes of krex_inject. */
+#define KREX_INJ_ROUND 0 /* y = cvt(x + delta) */
+#define KREX_INJ_EXACT 1 /* x + delta if exact in the dtype, else x - delta, else x */
+
+/* Result of krex_check; 64 bytes, must be device-accessible. */
+typedef struct krex_check_result {
+    uint64_t n;            /* elements compared */
+    uint64_t mismatches;   /* elements not close, NaN ones included */
+    uint64_t nan_count;    /* elements with a NaN on either side */
+    uint64_t argmax_abs;   /* lowest index attaining max_abs; UINT64_MAX if none */
+    float max_abs;         /* max |a - b| over NaN-free elements (0 if none) */
+    float max_rel;         /* max |a - b| / |b| over NaN-free elements (0 if none) */
+    uint64_t reserved[3];  /* reduction scratch; unspecified after the call */
+} krex_check_result;
+
+/* --- process registration ------------------------------------------------
+ * Registers this process with the region coordinator of `device` (Section
+ * 4.2: each process registers before it submits GPU work). shm_name names
+ * the POSIX shared-memory segment shared by every process on that GPU (NULL:
+ * "/krex-" + the device's PCI bus id). The first process creates and
+ * initialises it. flags: KREX_ATTACH_NO_GATE registers without gating (the
+ * ungated control configuration of Section 6.1); the process can still
+ * enter regions. Returns KREX_ESTATE if already attached, KREX_EPEER if the
+ * segment has another layout version, KREX_ESYS on a POSIX failure. */
+#define KREX_ATTACH_NO_GATE 1u
+krex_status krex_attach(int32_t device, const char *shm_name, uint32_t flags);
+
+/* Waits for this process's in-flight work, releases its slot and the
+ * mapping. Returns KREX_ESTATE inside a region or when not attached. */
+krex_status krex_detach(void);
+
+/* --- generation -----------------------------------------------------------
+ * Fills dst[0..n) (device, dtype `dtype`, aligned to its element size) with
+ * element j = transform(W_seed[offset + j]), where W_s[w] is output lane
+ * w mod 4 of Philox4x32-10 (Salmon et al., SC'11) with key
+ * (seed mod 2^32, seed >> 32) and counter (b mod 2^32, b >> 32, 0, 0),
+ * b = w >> 2. This is the input generation of a benchmarking command
+ * (Section 1; Section 2.1); being counter-based, it is independent of
+ * launch shape, timing and colocated work (Section 2.1, "Benchmarking
+ * command"). KREX_NORMAL pairs words (2p, 2p + 1), p = w >> 1, and element w
+ * takes the cosine branch when w is even, the sine branch when odd.
+ * Conversions to bf16 / fp16 / fp8 round to nearest even; fp8 is
+ * non-saturating (NaN beyond 448). KREX_U32 stores the words and ignores
+ * dist, p0, p1. Requires offset + n <= 2^64; uniform: finite p0 <= p1 with
+ * finite p1 - p0; normal: finite p0, finite p1 >= 0. */
+krex_status krex_gen(void *dst, int32_t dtype, uint64_t n, uint64_t seed, uint64_t offset,
+                     int32_t dist, float p0, float p1, void *stream);
+
+/* Same transforms applied to caller-supplied words: element j of dst is
+ * transform(words[j]) (normal: pairs (words[2p], words[2p + 1]); n even).
+ * words: device, n uint32 values. */
+krex_status krex_transform_words(void *dst, int32_t dtype, uint64_t n, const uint32_t *words,
+                                 int32_t dist, float p0, float p1, void *stream);
+
+/* --- mismatch injection ---------------------------------------------------
+ * y[i] = perturbed x[i] where W_mask_seed[mask_offset + i] < floor(rate 2^32)
+ * (a Bernoulli mask on its own word stream), else x[i]. ROUND: cvt(x + delta).
+ * EXACT: x + delta if both the fp32 sum and its conversion are exact, else
+ * x - delta under the same test, else x unchanged. y may equal x (in place)
+ * but must not otherwise overlap it. Stands in for a candidate's wrong
+ * outputs so the check's verdict is known (Section 2.1). rate in [0, 1],
+ * delta finite, dtype not KREX_U32. */
+krex_status krex_inject(void *y, const void *x, int32_t dtype, uint64_t n, uint64_t mask_seed,
+                        uint64_t mask_offset, double rate, float delta, int32_t mode, void *stream);
+
+/* --- correctness check ----------------------------------------------------
+ * Compares a (candidate, dtype dta) with b (reference, dtype dtb), n elements
+ * each, device memory, and writes *out (device-accessible; overwritten, no
+ * need to clear it). Per element, both sides are upcast to fp32 (exact):
+ * NaN on either side -> mismatch, counted in nan_count, left out of the
+ * maxima; a == b -> close, d = 0, rel = 0; else an infinity on either side
+ * -> mismatch, d = rel = +inf; else d = |a - b|, close iff
+ * d <= atol + rtol |b| (fp32, two roundings), rel = d / |b|. The check of a
+ * benchmarking command (Section 1; Section 2.1). rtol, atol finite >= 0;
+ * n < 2^33; a and b aligned to their element sizes. n = 0 writes the empty
+ * result. The result is ready when the stream reaches it. */
+krex_status krex_check(const void *a, int32_t dta, const void *b, int32_t dtb, uint64_t n, float rtol,
+                       float atol, krex_check_result *out, void *stream);
+
+/* --- cache flush ------------------------------------------------------------
+ * Writes `pattern` to every 32-bit word of buf[0..bytes) (device, 16-byte
+ * aligned, bytes a multiple of 16) with ordinary allocating stores, evicting
+ * earlier contents of the L2 and Infinity Cache when bytes exceeds their
+ * size (Section 2.1: flush between timed iterations; Section 4.2 step 5:
+ * memset over a cache-sized buffer). */
+krex_status krex_flush(void *buf, uint64_t bytes, uint32_t pattern, void *stream);
+
+/* --- probe kernel -----------------------------------------------------------
+ * A known-work timed kernel: 256 blocks x 256 threads, each thread runs 8
+ * independent fp32 FMA chains for `iters` steps and writes their sum to
+ * sink[thread] (device, 65536 floats). Used to measure timing inflation
+ * (Section 6.3, Eq. 1). */
+#define KREX_PROBE_THREADS 65536
+krex_status krex_probe(uint64_t iters, float *sink, void *stream);
+
+/* --- critical region --------------------------------------------------------
+ * Begins a critical region on this process's GPU (Section 4.1; Section 4.2):
+ * waits for this process's own earlier GPU work, takes the region lock
+ * (step 1), closes the gate with this process as holder and a new epoch
+ * (step 2), waits until every other registered process has no work in
+ * flight (step 3, completion counters of Section 5), then, if flush_buf is
+ * non-NULL, flushes flush_bytes of it on `stream` and waits for it (step 5).
+ * Fails without entering (gate reopened, lock released) on timeout, on a
+ * HIP error or if the lock cannot be taken within timeout_ms (Section 4.2:
+ * a failed entry starts no measurement). Returns KREX_RECOVERED when the
+ * lock was taken over from a holder that died inside its region.
+ * KREX_ENOTATTACHED without krex_attach; KREX_ESTATE when already inside. */
+krex_status krex_region_begin(void *stream, uint32_t timeout_ms, void *flush_buf, uint64_t flush_bytes);
+
+/* Ends the region: waits for this process's region work to finish on the
+ * device, reopens the gate, wakes parked siblings and releases the lock
+ * (Section 4.2, step 8). KREX_ESTATE when not inside a region. */
+krex_status krex_region_end(void *stream);
+
+/* --- timed loop ---------------------------------------------------------------
+ * do_bench-style loop (Section 2.1; Triton's do_bench, Section 8): `warmup`
+ * untimed calls of fn(user, stream), then `reps` times: flush flush_bytes of
+ * flush_buf with pattern 0x9E3779B9 * (rep + 1) (if flush_buf is non-NULL),
+ * record a start event, fn(user, stream), record an end event; one
+ * synchronisation at the end. times_ms[rep] (host, reps entries) receives
+ * each rep's start-to-end time; flush_ms (host, optional) each flush's
+ * time. With KREX_TL_REGION the whole loop, warm-up included, runs inside a
+ * critical region (Section 4.1: the region holds the warm-up and the timed
+ * loop, not the checks), entered with timeout_ms. reps >= 1. */
+typedef void (*krex_launch_fn)(void *user, void *stream);
+#define KREX_TL_REGION 1u
+krex_status krex_time_loop(krex_launch_fn fn, void *user, uint32_t warmup, uint32_t reps, void *flush_buf,
+                           uint64_t flush_bytes, uint32_t flags, uint32_t timeout_ms, void *stream,
+                           float *times_ms, float *flush_ms);
+
+/* Ready-made launch functions for krex_time_loop. */
+typedef struct krex_probe_args {
+    uint64_t iters;
+    float *sink;          /* device, KREX_PROBE_THREADS floats */
+} krex_probe_args;
+void krex_probe_launch(void *user /* krex_probe_args* */, void *stream);
+
+/* Naive fp32 GEMM, row-major C[M x N] = A[M x K] B[K x N], each element an
+ * fma chain over k ascending from +0: the candidate kernel of the tiny GEMM
+ * benchmarking command (a stand-in for an agent's kernel, Section 2.1). */
+typedef struct krex_sgemm_args {
+    uint32_t M, N, K;
+    const float *A, *B;   /* device */
+    float *C;             /* device */
+} krex_sgemm_args;
+krex_status krex_fixture_sgemm(uint32_t M, uint32_t N, uint32_t K, const float *A, const float *B, float *C,
+                               void *stream);
+void krex_sgemm_launch(void *user /* krex_sgemm_args* */, void *stream);
+
+/* --- introspection ----------------------------------------------------------- */
+typedef struct krex_gate_stats {
+    uint64_t regions;          /* regions entered by this process */
+    uint64_t last_drain_ns;    /* gate closed -> siblings drained, last entry */
+    uint64_t total_drain_ns;
+    uint64_t parks;            /* submissions of this process that waited at a closed gate */
+    uint64_t park_ns;          /* time spent waiting there */
+    uint64_t recoveries;       /* dead holders recovered by this process */
+    int32_t slot;              /* this process's registration slot, -1 if none */
+    int32_t gated;             /* 1 if submissions are gated */
+} krex_gate_stats;
+krex_status krex_get_gate_stats(krex_gate_stats *out /* host */);
+
+const char *krex_strerror(krex_status st);
+int32_t krex_last_hip_error(void);
+const char *krex_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KREX_H */

@@ -24,7 +24,7 @@ import numpy as np
 from . import build as _build
 
 F32, BF16, F16, F8E4M3, U32 = 0, 1, 2, 3, 4
-UNIFORM, NORMAL = 0, 1
+UNIFORM, NORMAL, BITCAST = 0, 1, 2
 INJ_ROUND, INJ_EXACT = 0, 1
 
 DTYPE_NAMES = {"f32": F32, "bf16": BF16, "f16": F16, "f8": F8E4M3, "u32": U32}
@@ -58,6 +58,9 @@ def lib():
         L.ko_gen.argtypes = [vp, ctypes.c_int, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64,
                              ctypes.c_int, ctypes.c_float, ctypes.c_float]
         L.ko_gen.restype = ctypes.c_int
+        L.ko_transform_words.argtypes = [vp, ctypes.c_int, ctypes.c_uint64, vp, ctypes.c_int,
+                                         ctypes.c_float, ctypes.c_float]
+        L.ko_transform_words.restype = ctypes.c_int
         L.ko_inject.argtypes = [vp, vp, ctypes.c_int, ctypes.c_uint64, ctypes.c_uint64,
                                 ctypes.c_uint64, ctypes.c_double, ctypes.c_float, ctypes.c_int]
         L.ko_inject.restype = ctypes.c_int64
@@ -121,6 +124,16 @@ def gen(dt, n, seed, offset=0, dist=UNIFORM, p0=-1.0, p1=1.0):
     st = lib().ko_gen(_ptr(out), dt, n, seed, offset, dist, p0, p1)
     if st != 0:
         raise ValueError("ko_gen rejected its arguments (%d)" % st)
+    return out
+
+
+def transform_words(dt, words_, dist=UNIFORM, p0=-1.0, p1=1.0):
+    dt = dtype_code(dt)
+    w = np.ascontiguousarray(words_, dtype=np.uint32)
+    out = np.empty(w.size, dtype=NP_STORAGE[dt])
+    st = lib().ko_transform_words(_ptr(out), dt, w.size, _ptr(w), dist, p0, p1)
+    if st != 0:
+        raise ValueError("ko_transform_words rejected its arguments (%d)" % st)
     return out
 
 

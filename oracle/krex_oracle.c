@@ -37,6 +37,7 @@
  *            with this file's own fp32 ln, sin/cos(2 pi k / 2^24) and the
  *            IEEE square root; element w takes the cosine branch if w is
  *            even, the sine branch if odd; v = mu + sigma * z.
+ *   bitcast  v = the word's 32 bits read as an fp32 value (any pattern).
  *   convert  fp32 -> bf16 / fp16 / fp8-e4m3fn, round to nearest even,
  *            subnormals kept; fp8 is non-saturating (beyond 448 -> NaN).
  *   check    b is the reference: per element, upcast both to fp32; NaN on
@@ -62,6 +63,7 @@
 
 #define KO_UNIFORM 0
 #define KO_NORMAL 1
+#define KO_BITCAST 2
 
 #define KO_INJ_ROUND 0
 #define KO_INJ_EXACT 1
@@ -421,10 +423,21 @@ void ko_normal_pair(uint32_t w0, uint32_t w1, float *z0, float *z1)
  * Generation: element j of dst gets word offset + j, transformed and
  * rounded to dt. KO_U32 stores the raw words.
  * ---------------------------------------------------------------------- */
+static int params_ok(int dist, float p0, float p1)
+{
+    if (dist == KO_UNIFORM)
+        return isfinite(p0) && isfinite(p1) && p0 <= p1 && isfinite(p1 - p0);
+    if (dist == KO_NORMAL)
+        return isfinite(p0) && isfinite(p1) && p1 >= 0.0f;
+    return dist == KO_BITCAST;
+}
+
 int ko_gen(void *dst, int dt, uint64_t n, uint64_t seed, uint64_t offset,
            int dist, float p0, float p1)
 {
-    if (dtype_size(dt) == 0 || (dist != KO_UNIFORM && dist != KO_NORMAL))
+    if (dtype_size(dt) == 0)
+        return KO_EINVAL;
+    if (dt != KO_U32 && !params_ok(dist, p0, p1))
         return KO_EINVAL;
     if (n > 0 && offset > UINT64_MAX - (n - 1))
         return KO_EINVAL;
@@ -438,6 +451,8 @@ int ko_gen(void *dst, int dt, uint64_t n, uint64_t seed, uint64_t offset,
         float v;
         if (dist == KO_UNIFORM) {
             v = ko_uniform(W, p0, p1);
+        } else if (dist == KO_BITCAST) {
+            v = u2f(W);
         } else {
             uint64_t wp = w & ~(uint64_t)1;  /* first word of the pair */
             uint32_t w0 = ko_word(seed, wp);
@@ -445,6 +460,40 @@ int ko_gen(void *dst, int dt, uint64_t n, uint64_t seed, uint64_t offset,
             float z0, z1;
             ko_normal_pair(w0, w1, &z0, &z1);
             float z = (w & 1u) ? z1 : z0;
+            float sz = p1 * z;
+            v = p0 + sz;
+        }
+        store_f32(dst, dt, j, v);
+    }
+    return KO_OK;
+}
+
+/* The same transforms on caller-supplied words: element j uses words[j];
+ * the normal pair of element j is (words[j & ~1], words[j | 1]). */
+int ko_transform_words(void *dst, int dt, uint64_t n, const uint32_t *words,
+                       int dist, float p0, float p1)
+{
+    if (dtype_size(dt) == 0)
+        return KO_EINVAL;
+    if (dt != KO_U32 && !params_ok(dist, p0, p1))
+        return KO_EINVAL;
+    if (dist == KO_NORMAL && dt != KO_U32 && (n & 1u))
+        return KO_EINVAL;
+    for (uint64_t j = 0; j < n; ++j) {
+        uint32_t W = words[j];
+        if (dt == KO_U32) {
+            ((uint32_t *)dst)[j] = W;
+            continue;
+        }
+        float v;
+        if (dist == KO_UNIFORM) {
+            v = ko_uniform(W, p0, p1);
+        } else if (dist == KO_BITCAST) {
+            v = u2f(W);
+        } else {
+            float z0, z1;
+            ko_normal_pair(words[j & ~(uint64_t)1], words[j | 1u], &z0, &z1);
+            float z = (j & 1u) ? z1 : z0;
             float sz = p1 * z;
             v = p0 + sz;
         }

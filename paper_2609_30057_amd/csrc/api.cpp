@@ -1,0 +1,525 @@
+// api.cpp -- the C ABI of include/krex.h: argument validation, counter-and-
+// gate around every launch, device-completion tracking of counted work,
+// region entry and exit, and the timed loop.
+//
+// Completion tracking follows the AMD variant of the paper (Section 5): the
+// in-flight counter is incremented when an operation is admitted and
+// decremented by a polling thread when the operation's completion signal
+// fires; here the signal is a HIP event recorded after the launch and the
+// thread blocks on it. A failed launch releases its count at once (Section
+// 4.2: decrement on error returns too).
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <atomic>
+#include <chrono>
+#include <condition_variable>
+#include <deque>
+#include <mutex>
+#include <thread>
+#include <vector>
+
+#include "gate.hpp"
+#include "krex.h"
+#include "launch.hpp"
+
+namespace {
+
+thread_local int32_t g_last_hip = 0;
+thread_local hipError_t g_fn_error = hipSuccess;   // set by the ready-made launch functions
+
+krex_status hip_fail(hipError_t e)
+{
+    g_last_hip = (int32_t)e;
+    return KREX_EHIP;
+}
+
+size_t elem_size(int32_t dt)
+{
+    switch (dt) {
+    case KREX_F32: return 4;
+    case KREX_BF16: return 2;
+    case KREX_F16: return 2;
+    case KREX_F8E4M3: return 1;
+    case KREX_U32: return 4;
+    default: return 0;
+    }
+}
+
+bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+int current_device()
+{
+    int d = 0;
+    if (hipGetDevice(&d) != hipSuccess) return 0;
+    return d;
+}
+
+// ------------------------------------------------------------ completion tracking
+
+class Tracker {
+public:
+    // Records a completion event for counted work on `s` and hands it to the
+    // tracking thread. On failure the count is released here.
+    krex_status track(hipStream_t s)
+    {
+        const int dev = current_device();
+        hipEvent_t ev = take_event(dev);
+        hipError_t e = ev ? hipEventRecord(ev, s) : hipErrorOutOfMemory;
+        if (e != hipSuccess) {
+            if (ev) give_event(dev, ev);
+            krexg::release(1);
+            return hip_fail(e);
+        }
+        {
+            std::lock_guard<std::mutex> g(mu_);
+            q_.push_back({ev, dev});
+            pending_.fetch_add(1);
+            if (!started_) {
+                started_ = true;
+                th_ = std::thread([this] { run(); });
+                atexit([] { Tracker::instance().shutdown(); });
+            }
+        }
+        cv_.notify_one();
+        return KREX_OK;
+    }
+
+    // Waits (up to timeout_ms) until every tracked operation was released.
+    bool drain(uint32_t timeout_ms)
+    {
+        const auto end = std::chrono::steady_clock::now() + std::chrono::milliseconds(timeout_ms);
+        while (pending_.load() != 0) {
+            if (std::chrono::steady_clock::now() > end) return false;
+            std::this_thread::sleep_for(std::chrono::microseconds(50));
+        }
+        return true;
+    }
+
+    static Tracker &instance()
+    {
+        static Tracker *t = new Tracker();   // never destroyed; the thread is joined at exit
+        return *t;
+    }
+
+private:
+    struct Item {
+        hipEvent_t ev;
+        int dev;
+    };
+
+    hipEvent_t take_event(int dev)
+    {
+        std::lock_guard<std::mutex> g(pool_mu_);
+        if (dev >= 0 && dev < 64 && !pool_[dev].empty()) {
+            hipEvent_t ev = pool_[dev].back();
+            pool_[dev].pop_back();
+            return ev;
+        }
+        hipEvent_t ev = nullptr;
+        if (hipEventCreateWithFlags(&ev, hipEventDisableTiming | hipEventBlockingSync) != hipSuccess) return nullptr;
+        return ev;
+    }
+
+    void give_event(int dev, hipEvent_t ev)
+    {
+        std::lock_guard<std::mutex> g(pool_mu_);
+        if (dev >= 0 && dev < 64) pool_[dev].push_back(ev);
+        else hipEventDestroy(ev);
+    }
+
+    void run()
+    {
+        int cur = -1;
+        for (;;) {
+            Item it;
+            {
+                std::unique_lock<std::mutex> g(mu_);
+                cv_.wait(g, [this] { return !q_.empty() || stop_; });
+                if (q_.empty()) return;   // stop requested and nothing left
+                it = q_.front();
+                q_.pop_front();
+            }
+            if (it.dev != cur) {
+                hipSetDevice(it.dev);
+                cur = it.dev;
+            }
+            hipEventSynchronize(it.ev);
+            krexg::release(1);
+            give_event(it.dev, it.ev);
+            pending_.fetch_sub(1);
+        }
+    }
+
+    void shutdown()
+    {
+        {
+            std::lock_guard<std::mutex> g(mu_);
+            stop_ = true;
+        }
+        cv_.notify_all();
+        if (th_.joinable()) th_.join();
+    }
+
+    std::mutex mu_;
+    std::condition_variable cv_;
+    std::deque<Item> q_;
+    std::thread th_;
+    bool started_ = false;
+    bool stop_ = false;
+    std::atomic<int64_t> pending_{0};
+    std::mutex pool_mu_;
+    std::vector<hipEvent_t> pool_[64];
+};
+
+uint64_t gate_timeout_ns()
+{
+    static uint64_t t = [] {
+        const char *e = getenv("KREX_GATE_TIMEOUT_MS");
+        return e ? (uint64_t)strtoull(e, nullptr, 10) * 1000000ull : 0ull;
+    }();
+    return t;
+}
+
+// Counter-and-gate around one submission: admit, launch, then either track
+// its completion or release it at once on failure.
+template <typename F>
+krex_status submit(hipStream_t s, F &&launch_fn)
+{
+    bool counted = false;
+    const int rc = krexg::admit(gate_timeout_ns(), &counted);
+    if (rc != KREX_OK) return rc;
+    const hipError_t e = launch_fn();
+    if (e != hipSuccess) {
+        if (counted) krexg::release(1);
+        return hip_fail(e);
+    }
+    if (counted) return Tracker::instance().track(s);
+    return KREX_OK;
+}
+
+// Cached timing events for the timed loop, per device.
+std::mutex g_ev_mu;
+std::vector<hipEvent_t> g_timing_events[64];
+
+krex_status timing_events(int dev, size_t count, hipEvent_t **out)
+{
+    if (dev < 0 || dev >= 64) return KREX_EINVAL;
+    std::vector<hipEvent_t> &v = g_timing_events[dev];
+    while (v.size() < count) {
+        hipEvent_t ev;
+        hipError_t e = hipEventCreate(&ev);
+        if (e != hipSuccess) return hip_fail(e);
+        v.push_back(ev);
+    }
+    *out = v.data();
+    return KREX_OK;
+}
+
+bool finite_f(float x) { return isfinite(x) != 0; }
+
+bool gen_params_ok(int32_t dist, float p0, float p1)
+{
+    if (dist == KREX_UNIFORM) return finite_f(p0) && finite_f(p1) && p0 <= p1 && finite_f(p1 - p0);
+    if (dist == KREX_NORMAL) return finite_f(p0) && finite_f(p1) && p1 >= 0.0f;
+    return dist == KREX_BITCAST;
+}
+
+int32_t g_device_attached = -1;
+
+}  // namespace
+
+namespace krex {
+
+int device_cus()
+{
+    static std::atomic<int> cache[64];
+    const int dev = current_device();
+    if (dev < 0 || dev >= 64) return 256;
+    int v = cache[dev].load();
+    if (v == 0) {
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
+        cache[dev].store(v);
+    }
+    return v;
+}
+
+}  // namespace krex
+
+extern "C" {
+
+krex_status krex_attach(int32_t device, const char *shm_name, uint32_t flags)
+{
+    if (flags & ~KREX_ATTACH_NO_GATE) return KREX_EINVAL;
+    char name[256];
+    if (shm_name) {
+        if (strlen(shm_name) >= sizeof name) return KREX_EINVAL;
+        strcpy(name, shm_name);
+    } else {
+        char bus[64];
+        hipError_t e = hipDeviceGetPCIBusId(bus, (int)sizeof bus, device);
+        if (e != hipSuccess) return hip_fail(e);
+        for (char *p = bus; *p; ++p)
+            if (*p == ':' || *p == '.') *p = '_';
+        snprintf(name, sizeof name, "/krex-%s", bus);
+    }
+    const int rc = krexg::attach(name, (flags & KREX_ATTACH_NO_GATE) ? krexg::kNoGate : 0u);
+    if (rc == KREX_OK) g_device_attached = device;
+    return rc;
+}
+
+krex_status krex_detach(void)
+{
+    if (!krexg::attached()) return KREX_ESTATE;
+    if (krexg::in_region()) return KREX_ESTATE;
+    if (!Tracker::instance().drain(60000)) return KREX_ETIMEDOUT;
+    const int rc = krexg::detach();
+    if (rc == KREX_OK) g_device_attached = -1;
+    return rc;
+}
+
+krex_status krex_gen(void *dst, int32_t dtype, uint64_t n, uint64_t seed, uint64_t offset, int32_t dist, float p0,
+                     float p1, void *stream)
+{
+    const size_t es = elem_size(dtype);
+    if (es == 0) return KREX_EINVAL;
+    if (dtype != KREX_U32 && !gen_params_ok(dist, p0, p1)) return KREX_EINVAL;
+    if (n > 0 && offset > UINT64_MAX - (n - 1)) return KREX_EINVAL;
+    if (n > 0 && !dst) return KREX_EINVAL;
+    if (!aligned(dst, es)) return KREX_EALIGN;
+    if (n == 0) return KREX_OK;
+    hipStream_t s = (hipStream_t)stream;
+    return submit(s, [&] { return krex::launch_gen(dst, dtype, n, seed, offset, dist, p0, p1, s); });
+}
+
+krex_status krex_transform_words(void *dst, int32_t dtype, uint64_t n, const uint32_t *words, int32_t dist, float p0,
+                                 float p1, void *stream)
+{
+    const size_t es = elem_size(dtype);
+    if (es == 0) return KREX_EINVAL;
+    if (dtype != KREX_U32 && !gen_params_ok(dist, p0, p1)) return KREX_EINVAL;
+    if (dtype != KREX_U32 && dist == KREX_NORMAL && (n & 1u)) return KREX_EINVAL;
+    if (n > 0 && (!dst || !words)) return KREX_EINVAL;
+    if (!aligned(dst, es) || !aligned(words, 4)) return KREX_EALIGN;
+    if (n == 0) return KREX_OK;
+    hipStream_t s = (hipStream_t)stream;
+    return submit(s, [&] { return krex::launch_xform(dst, dtype, n, words, dist, p0, p1, s); });
+}
+
+krex_status krex_inject(void *y, const void *x, int32_t dtype, uint64_t n, uint64_t mask_seed, uint64_t mask_offset,
+                        double rate, float delta, int32_t mode, void *stream)
+{
+    const size_t es = elem_size(dtype);
+    if (es == 0 || dtype == KREX_U32) return KREX_EINVAL;
+    if (!(rate >= 0.0 && rate <= 1.0)) return KREX_EINVAL;
+    if (!finite_f(delta)) return KREX_EINVAL;
+    if (mode != KREX_INJ_ROUND && mode != KREX_INJ_EXACT) return KREX_EINVAL;
+    if (n > 0 && mask_offset > UINT64_MAX - (n - 1)) return KREX_EINVAL;
+    if (n > 0 && (!x || !y)) return KREX_EINVAL;
+    if (!aligned(x, es) || !aligned(y, es)) return KREX_EALIGN;
+    if (n == 0) return KREX_OK;
+    if (x != y) {
+        const uintptr_t xa = (uintptr_t)x, ya = (uintptr_t)y, len = (uintptr_t)(n * es);
+        if (xa < ya + len && ya < xa + len) return KREX_EINVAL;   // partial overlap
+    }
+    double t = floor(rate * 4294967296.0);
+    const uint64_t T = t <= 0.0 ? 0ull : (t >= 4294967296.0 ? (1ull << 32) : (uint64_t)t);
+    hipStream_t s = (hipStream_t)stream;
+    return submit(s, [&] { return krex::launch_inject(y, x, dtype, n, mask_seed, mask_offset, T, delta, mode, s); });
+}
+
+krex_status krex_check(const void *a, int32_t dta, const void *b, int32_t dtb, uint64_t n, float rtol, float atol,
+                       krex_check_result *out, void *stream)
+{
+    const size_t sa = elem_size(dta), sb = elem_size(dtb);
+    if (sa == 0 || sb == 0 || dta == KREX_U32 || dtb == KREX_U32) return KREX_EINVAL;
+    if (!(rtol >= 0.0f) || !(atol >= 0.0f) || !finite_f(rtol) || !finite_f(atol)) return KREX_EINVAL;
+    if (n >= (1ull << 33)) return KREX_EINVAL;
+    if (!out) return KREX_EINVAL;
+    if (n > 0 && (!a || !b)) return KREX_EINVAL;
+    if (!aligned(a, sa) || !aligned(b, sb) || !aligned(out, 8)) return KREX_EALIGN;
+    hipStream_t s = (hipStream_t)stream;
+    return submit(s, [&] { return krex::launch_check(a, dta, b, dtb, n, rtol, atol, out, s); });
+}
+
+krex_status krex_flush(void *buf, uint64_t bytes, uint32_t pattern, void *stream)
+{
+    if (bytes % 16 != 0) return KREX_EINVAL;
+    if (bytes > 0 && !buf) return KREX_EINVAL;
+    if (!aligned(buf, 16)) return KREX_EALIGN;
+    if (bytes == 0) return KREX_OK;
+    hipStream_t s = (hipStream_t)stream;
+    return submit(s, [&] { return krex::launch_flush(buf, bytes, pattern, s); });
+}
+
+krex_status krex_probe(uint64_t iters, float *sink, void *stream)
+{
+    if (!sink) return KREX_EINVAL;
+    if (!aligned(sink, 4)) return KREX_EALIGN;
+    hipStream_t s = (hipStream_t)stream;
+    return submit(s, [&] { return krex::launch_probe(iters, sink, s); });
+}
+
+krex_status krex_fixture_sgemm(uint32_t M, uint32_t N, uint32_t K, const float *A, const float *B, float *C,
+                               void *stream)
+{
+    if ((uint64_t)M * N > 0 && (!C || (K > 0 && (!A || !B)))) return KREX_EINVAL;
+    if (!aligned(A, 4) || !aligned(B, 4) || !aligned(C, 4)) return KREX_EALIGN;
+    hipStream_t s = (hipStream_t)stream;
+    return submit(s, [&] { return krex::launch_sgemm(M, N, K, A, B, C, s); });
+}
+
+void krex_probe_launch(void *user, void *stream)
+{
+    const krex_probe_args *a = (const krex_probe_args *)user;
+    const hipError_t e = krex::launch_probe(a->iters, a->sink, (hipStream_t)stream);
+    if (e != hipSuccess && g_fn_error == hipSuccess) g_fn_error = e;
+}
+
+void krex_sgemm_launch(void *user, void *stream)
+{
+    const krex_sgemm_args *a = (const krex_sgemm_args *)user;
+    const hipError_t e = krex::launch_sgemm(a->M, a->N, a->K, a->A, a->B, a->C, (hipStream_t)stream);
+    if (e != hipSuccess && g_fn_error == hipSuccess) g_fn_error = e;
+}
+
+krex_status krex_region_begin(void *stream, uint32_t timeout_ms, void *flush_buf, uint64_t flush_bytes)
+{
+    if (!krexg::attached()) return KREX_ENOTATTACHED;
+    if (krexg::in_region()) return KREX_ESTATE;
+    if (flush_buf && (flush_bytes % 16 != 0 || !aligned(flush_buf, 16))) return KREX_EINVAL;
+    // This process's own earlier work finishes before the region starts.
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) return hip_fail(e);
+    const int rc = krexg::region_begin(timeout_ms);
+    if (rc < 0) return rc;
+    if (flush_buf && flush_bytes) {
+        hipStream_t s = (hipStream_t)stream;
+        e = krex::launch_flush(flush_buf, flush_bytes, 0u, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) {
+            krexg::region_end();
+            return hip_fail(e);
+        }
+    }
+    return rc;
+}
+
+krex_status krex_region_end(void *stream)
+{
+    (void)stream;
+    if (!krexg::attached()) return KREX_ENOTATTACHED;
+    if (!krexg::in_region()) return KREX_ESTATE;
+    // The region's work (on any stream of this process) finishes before the
+    // gate reopens; the region is left even if that wait reports an error.
+    const hipError_t e = hipDeviceSynchronize();
+    const int rc = krexg::region_end();
+    if (e != hipSuccess) return hip_fail(e);
+    return rc;
+}
+
+krex_status krex_time_loop(krex_launch_fn fn, void *user, uint32_t warmup, uint32_t reps, void *flush_buf,
+                           uint64_t flush_bytes, uint32_t flags, uint32_t timeout_ms, void *stream, float *times_ms,
+                           float *flush_ms)
+{
+    if (!fn || reps == 0 || !times_ms) return KREX_EINVAL;
+    if (flags & ~KREX_TL_REGION) return KREX_EINVAL;
+    if (flush_buf && (flush_bytes % 16 != 0 || flush_bytes == 0)) return KREX_EINVAL;
+    if (flush_buf && !aligned(flush_buf, 16)) return KREX_EALIGN;
+    const bool region = (flags & KREX_TL_REGION) != 0;
+    if (region && !krexg::attached()) return KREX_ENOTATTACHED;
+    if (region && krexg::in_region()) return KREX_ESTATE;
+    hipStream_t s = (hipStream_t)stream;
+    const int dev = current_device();
+    std::lock_guard<std::mutex> evg(g_ev_mu);
+    hipEvent_t *ev = nullptr;
+    krex_status rc = timing_events(dev, (size_t)reps * 3, &ev);
+    if (rc != KREX_OK) return rc;
+    hipEvent_t *ev_flush = ev, *ev_start = ev + reps, *ev_end = ev + 2 * (size_t)reps;
+
+    bool counted = false;
+    krex_status entry = KREX_OK;
+    if (region) {
+        entry = krex_region_begin(stream, timeout_ms, nullptr, 0);
+        if (entry < 0) return entry;   // a failed entry starts no measurement
+    } else {
+        rc = krexg::admit(gate_timeout_ns(), &counted);
+        if (rc != KREX_OK) return rc;
+    }
+    g_fn_error = hipSuccess;
+    hipError_t e = hipSuccess;
+    for (uint32_t w = 0; w < warmup && e == hipSuccess; ++w) {
+        fn(user, stream);
+        e = g_fn_error;
+    }
+    for (uint32_t r = 0; r < reps && e == hipSuccess; ++r) {
+        if (flush_buf) {
+            e = hipEventRecord(ev_flush[r], s);
+            if (e == hipSuccess) e = krex::launch_flush(flush_buf, flush_bytes, 0x9E3779B9u * (r + 1u), s);
+        }
+        if (e == hipSuccess) e = hipEventRecord(ev_start[r], s);
+        if (e == hipSuccess) {
+            fn(user, stream);
+            e = g_fn_error;
+        }
+        if (e == hipSuccess) e = hipEventRecord(ev_end[r], s);
+    }
+    if (e == hipSuccess) e = hipEventSynchronize(ev_end[reps - 1]);
+    for (uint32_t r = 0; r < reps && e == hipSuccess; ++r) {
+        e = hipEventElapsedTime(&times_ms[r], ev_start[r], ev_end[r]);
+        if (e == hipSuccess && flush_ms) e = flush_buf ? hipEventElapsedTime(&flush_ms[r], ev_flush[r], ev_start[r])
+                                                       : (flush_ms[r] = 0.0f, hipSuccess);
+    }
+    if (region) {
+        const krex_status end = krex_region_end(stream);
+        if (e == hipSuccess && end < 0) return end;
+    } else {
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (counted) krexg::release(1);
+    }
+    if (e != hipSuccess) return hip_fail(e);
+    return entry;
+}
+
+krex_status krex_get_gate_stats(krex_gate_stats *out)
+{
+    if (!out) return KREX_EINVAL;
+    krexg::Stats st;
+    krexg::get_stats(&st);
+    out->regions = st.regions;
+    out->last_drain_ns = st.last_drain_ns;
+    out->total_drain_ns = st.total_drain_ns;
+    out->parks = st.parks;
+    out->park_ns = st.park_ns;
+    out->recoveries = st.recoveries;
+    out->slot = st.slot;
+    out->gated = st.gated;
+    return KREX_OK;
+}
+
+const char *krex_strerror(krex_status st)
+{
+    switch (st) {
+    case KREX_OK: return "ok";
+    case KREX_RECOVERED: return "ok (region lock recovered from a dead holder)";
+    case KREX_EINVAL: return "invalid argument";
+    case KREX_EALIGN: return "misaligned pointer";
+    case KREX_EHIP: return "HIP runtime error";
+    case KREX_ETIMEDOUT: return "timed out";
+    case KREX_ESTATE: return "invalid state for this call";
+    case KREX_ENOTATTACHED: return "process not attached to a region coordinator";
+    case KREX_ENOMEM: return "out of host memory";
+    case KREX_EPEER: return "shared segment unusable";
+    case KREX_ESYS: return "system call failed";
+    default: return "unknown status";
+    }
+}
+
+int32_t krex_last_hip_error(void) { return g_last_hip; }
+
+const char *krex_version(void) { return "krex-mi355x 0.1 (gfx950)"; }
+
+}  // extern "C"

@@ -1,0 +1,280 @@
+// krex_device.hpp -- device-side building blocks of the gfx950 hot path:
+// the Philox4x32-10 block function, the value transforms (uniform, Box-Muller
+// normal with own fp32 ln / sin / cos, bitcast) and round-to-nearest-even
+// narrowing to bf16 / fp16 / fp8-e4m3fn plus exact upcasts.
+//
+// Every definition here is the generation / check reading of the paper's
+// command phases (KREX, Section 1 and Section 2.1: generate inputs, check
+// against a reference, then time). The paper names no RNG or transform; the
+// stream is Philox4x32-10 (Salmon et al., SC'11) so that each element's value
+// is a pure function of (seed, offset + j), independent of launch shape and
+// of colocated work (Section 2.1, "Benchmarking command").
+//
+// All arithmetic is fp32 with contraction disabled at build time; a fused
+// multiply-add appears only where __builtin_fmaf is written. Division and
+// square root are the correctly rounded IEEE operations.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace krex {
+
+enum : int { F32 = 0, BF16 = 1, F16 = 2, F8 = 3, U32 = 4 };
+enum : int { UNIFORM = 0, NORMAL = 1, BITCAST = 2 };
+enum : int { INJ_ROUND = 0, INJ_EXACT = 1 };
+
+template <int DT> struct dtype_traits;
+template <> struct dtype_traits<F32> { using storage = uint32_t; static constexpr int size = 4; };
+template <> struct dtype_traits<BF16> { using storage = uint16_t; static constexpr int size = 2; };
+template <> struct dtype_traits<F16> { using storage = uint16_t; static constexpr int size = 2; };
+template <> struct dtype_traits<F8> { using storage = uint8_t; static constexpr int size = 1; };
+template <> struct dtype_traits<U32> { using storage = uint32_t; static constexpr int size = 4; };
+
+struct words4 {
+    uint32_t v[4];
+};
+
+// Philox4x32-10 on counter (c0, c1, 0, 0) with key (k0, k1). Per round the
+// two 32x32->64 products M0*x0 and M1*x2 are formed and the state becomes
+// (hi(M1 x2) ^ x1 ^ k0, lo(M1 x2), hi(M0 x0) ^ x3 ^ k1, lo(M0 x0)); the key
+// advances by the Weyl constants between rounds. The key is wave-uniform,
+// so its schedule lives in scalar registers.
+__device__ __forceinline__ words4 philox10(uint32_t c0, uint32_t c1, uint32_t k0, uint32_t k1)
+{
+    uint32_t x0 = c0, x1 = c1, x2 = 0u, x3 = 0u;
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint64_t p0 = (uint64_t)0xD2511F53u * (uint64_t)x0;
+        const uint64_t p1 = (uint64_t)0xCD9E8D57u * (uint64_t)x2;
+        const uint32_t n0 = (uint32_t)(p1 >> 32) ^ x1 ^ k0;
+        const uint32_t n1 = (uint32_t)p1;
+        const uint32_t n2 = (uint32_t)(p0 >> 32) ^ x3 ^ k1;
+        const uint32_t n3 = (uint32_t)p0;
+        x0 = n0; x1 = n1; x2 = n2; x3 = n3;
+        k0 += 0x9E3779B9u;
+        k1 += 0xBB67AE85u;
+    }
+    words4 o;
+    o.v[0] = x0; o.v[1] = x1; o.v[2] = x2; o.v[3] = x3;
+    return o;
+}
+
+__device__ __forceinline__ words4 philox_block(uint64_t b, uint32_t k0, uint32_t k1)
+{
+    return philox10((uint32_t)b, (uint32_t)(b >> 32), k0, k1);
+}
+
+// ---------------------------------------------------------------- narrowing
+
+__device__ __forceinline__ uint32_t rne_shift(uint32_t m, uint32_t s)
+{
+    // m / 2^s rounded to nearest, ties to even; s >= 1
+    if (s >= 32u) return 0u;
+    const uint32_t q = m >> s;
+    const uint32_t rem = m & ((1u << s) - 1u);
+    const uint32_t half = 1u << (s - 1u);
+    return q + ((rem > half || (rem == half && (q & 1u))) ? 1u : 0u);
+}
+
+__device__ __forceinline__ uint16_t to_bf16(float f)
+{
+    uint32_t x = __float_as_uint(f);
+    if ((x & 0x7FFFFFFFu) > 0x7F800000u) return 0x7FC0u;
+    x += 0x7FFFu + ((x >> 16) & 1u);
+    return (uint16_t)(x >> 16);
+}
+
+__device__ __forceinline__ uint16_t to_f16(float f)
+{
+    const uint32_t x = __float_as_uint(f);
+    const uint32_t sign = (x >> 16) & 0x8000u;
+    const uint32_t ax = x & 0x7FFFFFFFu;
+    if (ax > 0x7F800000u) return 0x7E00u;
+    if (ax >= 0x477FF000u) return (uint16_t)(sign | 0x7C00u);          // rounds past 65504
+    if (ax >= 0x38800000u) {                                            // normal half
+        const uint32_t r = ax + 0xFFFu + ((ax >> 13) & 1u);
+        return (uint16_t)(sign | ((r - (112u << 23)) >> 13));
+    }
+    const uint32_t e = ax >> 23;                                        // units of 2^-24
+    if (e == 0u) return (uint16_t)sign;
+    return (uint16_t)(sign | rne_shift((ax & 0x7FFFFFu) | 0x800000u, 126u - e));
+}
+
+__device__ __forceinline__ uint8_t to_f8(float f)
+{
+    const uint32_t x = __float_as_uint(f);
+    const uint32_t sign = (x >> 24) & 0x80u;
+    const uint32_t ax = x & 0x7FFFFFFFu;
+    if (ax > 0x43E80000u) return (uint8_t)(sign | 0x7Fu);               // NaN, inf, > 464
+    if (ax >= 0x3C800000u) {                                            // normal e4m3
+        const uint32_t r = ax + 0x7FFFFu + ((ax >> 20) & 1u);
+        return (uint8_t)(sign | ((r - (120u << 23)) >> 20));
+    }
+    const uint32_t e = ax >> 23;                                        // units of 2^-9
+    if (e == 0u) return (uint8_t)sign;
+    return (uint8_t)(sign | rne_shift((ax & 0x7FFFFFu) | 0x800000u, 141u - e));
+}
+
+__device__ __forceinline__ float from_bf16(uint32_t h) { return __uint_as_float(h << 16); }
+
+__device__ __forceinline__ float from_f16(uint32_t h)
+{
+    const uint32_t sign = (h & 0x8000u) << 16;
+    const uint32_t e = (h >> 10) & 0x1Fu;
+    const uint32_t m = h & 0x3FFu;
+    if (e == 0x1Fu) return __uint_as_float(sign | 0x7F800000u | (m << 13));
+    if (e == 0u) {
+        const float v = (float)m * 0x1p-24f;
+        return sign ? -v : v;
+    }
+    return __uint_as_float(sign | ((e + 112u) << 23) | (m << 13));
+}
+
+__device__ __forceinline__ float from_f8(uint32_t h)
+{
+    const uint32_t sign = (h & 0x80u) << 24;
+    const uint32_t e = (h >> 3) & 0xFu;
+    const uint32_t m = h & 0x7u;
+    if (e == 0xFu && m == 0x7u) return __uint_as_float(sign | 0x7FC00000u);
+    if (e == 0u) {
+        const float v = (float)m * 0x1p-9f;
+        return sign ? -v : v;
+    }
+    return __uint_as_float(sign | ((e + 120u) << 23) | (m << 20));
+}
+
+template <int DT>
+__device__ __forceinline__ typename dtype_traits<DT>::storage narrow(float v)
+{
+    if constexpr (DT == F32) return __float_as_uint(v);
+    else if constexpr (DT == BF16) return to_bf16(v);
+    else if constexpr (DT == F16) return to_f16(v);
+    else return to_f8(v);
+}
+
+template <int DT>
+__device__ __forceinline__ float widen(uint32_t bits)
+{
+    if constexpr (DT == F32) return __uint_as_float(bits);
+    else if constexpr (DT == BF16) return from_bf16(bits);
+    else if constexpr (DT == F16) return from_f16(bits);
+    else return from_f8(bits);
+}
+
+// ---------------------------------------------------------------- fp32 math
+
+// ln x for a positive normal x: x = 2^e m, m in [sqrt(1/2), sqrt 2);
+// f = m - 1 (exact), s = f / (2 + f), ln m = 2 atanh s, written as
+// f - (f^2/2 - s (f^2/2 + R)) with R = z (2/3 + z (2/5 + z (2/7 + z (2/9 + z 2/11)))),
+// z = s^2; then e ln2 is added as e * head + (e * tail + ln m) with a
+// 16-bit head of ln 2.
+__device__ __forceinline__ float ln_f32(float x)
+{
+    const uint32_t ix = __float_as_uint(x);
+    int32_t e = (int32_t)(ix >> 23) - 127;
+    const uint32_t mb = ix & 0x7FFFFFu;
+    float m = __uint_as_float(mb | 0x3F800000u);
+    if (mb > 0x3504F3u) {
+        m = m * 0.5f;
+        e = e + 1;
+    }
+    const float f = m - 1.0f;
+    const float den = 2.0f + f;
+    const float s = f / den;
+    const float z = s * s;
+    float p = 0x1.745d18p-3f;
+    p = __builtin_fmaf(p, z, 0x1.c71c72p-3f);
+    p = __builtin_fmaf(p, z, 0x1.24924ap-2f);
+    p = __builtin_fmaf(p, z, 0x1.99999ap-2f);
+    p = __builtin_fmaf(p, z, 0x1.555556p-1f);
+    const float R = z * p;
+    const float hf = 0.5f * f;
+    const float hfsq = hf * f;
+    const float a = hfsq + R;
+    const float b = s * a;
+    const float c = hfsq - b;
+    const float lnm = f - c;
+    const float dk = (float)e;
+    const float tail = __builtin_fmaf(dk, 0x1.7f7d1cp-20f, lnm);
+    const float head = dk * 0x1.62e4p-1f;
+    return head + tail;
+}
+
+// sin and cos of 2 pi k 2^-24, k in [0, 2^24): quadrant q = round(k 2^-22),
+// r = (k - q 2^22) 2^-22 in [-1/2, 1/2) (exact integer steps), Taylor
+// polynomials of sin(pi r / 2) through r^9 and cos(pi r / 2) through r^10 in
+// Horner form on r^2, then the quadrant's swap and signs.
+__device__ __forceinline__ void sincos_2pi_q24(uint32_t k, float &sn, float &cs)
+{
+    const uint32_t q = (k + (1u << 21)) >> 22;
+    const int32_t ri = (int32_t)k - (int32_t)(q << 22);
+    const float r = (float)ri * 0x1p-22f;
+    const float y = r * r;
+    float ps = 0x1.507834p-13f;
+    ps = __builtin_fmaf(ps, y, -0x1.32d2ccp-8f);
+    ps = __builtin_fmaf(ps, y, 0x1.466bc6p-4f);
+    ps = __builtin_fmaf(ps, y, -0x1.4abbcep-1f);
+    ps = __builtin_fmaf(ps, y, 0x1.921fb6p+0f);
+    const float S = r * ps;
+    float pc = -0x1.a6d1f2p-16f;
+    pc = __builtin_fmaf(pc, y, 0x1.e1f506p-11f);
+    pc = __builtin_fmaf(pc, y, -0x1.55d3c8p-6f);
+    pc = __builtin_fmaf(pc, y, 0x1.03c1f0p-2f);
+    pc = __builtin_fmaf(pc, y, -0x1.3bd3ccp+0f);
+    const float C = __builtin_fmaf(pc, y, 1.0f);
+    switch (q & 3u) {
+    case 0: sn = S; cs = C; break;
+    case 1: sn = C; cs = -S; break;
+    case 2: sn = -S; cs = -C; break;
+    default: sn = -C; cs = S; break;
+    }
+}
+
+// Box-Muller on (w0, w1): u1 = ((w0 >> 8) + 1) 2^-24 in (0, 1],
+// rho = sqrt(0 - 2 ln u1) (so rho = +0 at u1 = 1), z0 = rho cos, z1 = rho sin
+// of 2 pi (w1 >> 8) 2^-24.
+__device__ __forceinline__ void normal_pair(uint32_t w0, uint32_t w1, float &z0, float &z1)
+{
+    const float u1 = (float)((w0 >> 8) + 1u) * 0x1p-24f;
+    const float L = ln_f32(u1);
+    const float t2 = 2.0f * L;
+    const float t = 0.0f - t2;
+    const float rho = __builtin_sqrtf(t);
+    float sn, cs;
+    sincos_2pi_q24(w1 >> 8, sn, cs);
+    z0 = rho * cs;
+    z1 = rho * sn;
+}
+
+__device__ __forceinline__ float uniform_f32(uint32_t w, float lo, float range)
+{
+    // range = fl(hi - lo), computed once on the host with the same rounding
+    const float u = (float)(w >> 8) * 0x1p-24f;
+    const float t = range * u;
+    return lo + t;
+}
+
+// Four values from four consecutive words (two normal pairs).
+template <int DIST>
+__device__ __forceinline__ void transform4(const words4 &w, float p0, float p1, float v[4])
+{
+    if constexpr (DIST == UNIFORM) {
+#pragma unroll
+        for (int l = 0; l < 4; ++l) v[l] = uniform_f32(w.v[l], p0, p1);
+    } else if constexpr (DIST == NORMAL) {
+        float z[4];
+        normal_pair(w.v[0], w.v[1], z[0], z[1]);
+        normal_pair(w.v[2], w.v[3], z[2], z[3]);
+#pragma unroll
+        for (int l = 0; l < 4; ++l) {
+            const float sz = p1 * z[l];
+            v[l] = p0 + sz;
+        }
+    } else {
+#pragma unroll
+        for (int l = 0; l < 4; ++l) v[l] = __uint_as_float(w.v[l]);
+    }
+}
+
+}  // namespace krex

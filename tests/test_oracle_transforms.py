@@ -181,3 +181,27 @@ def test_gen_rejects_bad_arguments(oracle_mod):
         oracle_mod.gen("f32", 10, 0, 2**64 - 5)                # offset + n wraps
     with pytest.raises(ValueError):
         oracle_mod.gen("f32", 10, 0, 0, 7)                     # unknown distribution
+
+
+def test_bitcast_is_the_word(oracle_mod):
+    w = oracle_mod.words(100000, 21, 5)
+    g = oracle_mod.gen("f32", 100000, 21, 5, oracle_mod.BITCAST, 0.0, 0.0)
+    assert np.array_equal(g.view(np.uint32), w)
+    h = oracle_mod.gen("f16", 100000, 21, 5, oracle_mod.BITCAST, 0.0, 0.0)
+    assert np.array_equal(h, oracle_mod.from_f32(w.view(np.float32), "f16"))
+
+
+def test_transform_words_equals_gen(oracle_mod):
+    for dist, p0, p1 in ((0, -1.0, 1.0), (1, 0.0, 1.0), (2, 0.0, 0.0)):
+        for dt in ("f32", "bf16", "f16", "f8", "u32"):
+            w = oracle_mod.words(4096, 77, 0)
+            got = oracle_mod.transform_words(dt, w, dist, p0, p1)
+            ref = oracle_mod.gen(dt, 4096, 77, 0, dist, p0, p1)
+            assert np.array_equal(got.view(np.uint8), ref.view(np.uint8))
+
+
+def test_gen_parameter_rules(oracle_mod):
+    for dist, p0, p1 in ((0, 1.0, -1.0), (0, float("nan"), 1.0), (0, -3e38, 3e38), (1, 0.0, -1.0),
+                         (1, float("inf"), 1.0)):
+        with pytest.raises(ValueError):
+            oracle_mod.gen("f32", 4, 0, 0, dist, p0, p1)
