@@ -18,6 +18,9 @@ measured by `--fidelity` (Section 6.3, Eq. 1), which prints its own line.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
        python bench.py --fidelity [--samples S]
+       python bench.py --kernels          per-kernel throughput on the command shapes
+       python bench.py --calib-copy       also time a plain 1 GiB device copy (the
+                                          reference kernel for rocprofv3 byte counters)
 """
 import argparse
 import hashlib
@@ -213,6 +216,76 @@ def run_gemm_large(steps, warmup, with_cpu):
     return out
 
 
+def run_kernels():
+    """Per-kernel throughput on the commands' shapes (median of 20 launches,
+    HIP events on the launching stream; includes the launch gaps)."""
+    import torch
+
+    import paper_2609_30057_amd as krex
+
+    def t_ms(fn, reps=20, warm=3):
+        for _ in range(warm):
+            fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            b.synchronize()
+            ts.append(a.elapsed_time(b))
+        ts.sort()
+        return ts[len(ts) // 2]
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    res = {}
+    N = 1 << 24
+
+    def rec(name, ms, nbytes):
+        res[name] = {"us": round(ms * 1e3, 1), "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                     "frac_hbm": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 3)}
+
+    x16 = torch.empty(N * 16, dtype=torch.float16, device=dev)
+    y16 = torch.empty_like(x16)
+    a_bf = torch.empty(N, dtype=torch.bfloat16, device=dev)
+    b_f32 = torch.empty(N, dtype=torch.float32, device=dev)
+    x8 = torch.empty(N * 16, dtype=torch.float8_e4m3fn, device=dev)
+    y8 = torch.empty_like(x8)
+    xf = torch.empty(N * 4, dtype=torch.float32, device=dev)
+    yf = torch.empty_like(xf)
+    fl = torch.empty(GIB // 4, dtype=torch.int32, device=dev)
+    out = krex.check_result_buffer()
+    rec("gen f16 uniform 268M", t_ms(lambda: krex.gen(x16, 2, 0, "uniform", -4.0, 4.0)), x16.numel() * 2)
+    rec("gen bf16 normal 16.8M", t_ms(lambda: krex.gen(a_bf, 1, 0, "normal")), N * 2)
+    rec("gen f32 normal 16.8M", t_ms(lambda: krex.gen(b_f32, 1, 0, "normal")), N * 4)
+    rec("gen f32 uniform 67M", t_ms(lambda: krex.gen(xf, 7, 0)), xf.numel() * 4)
+    rec("gen f8 normal 268M", t_ms(lambda: krex.gen(x8, 5, 0, "normal")), x8.numel())
+    rec("inject f16 exact 268M", t_ms(lambda: krex.inject(y16, x16, 3, 0.001, 0.5)), x16.numel() * 4)
+    krex.inject(y8, x8, 6, 0.01, 0.25, "round")
+    krex.inject(yf, xf, 8, 0.01, 0.5)
+    rec("check bf16xf32 16.8M", t_ms(lambda: krex.check(a_bf, b_f32, 1.6e-2, 1e-2, out=out, sync=False)), N * 6)
+    rec("check f16xf16 268M", t_ms(lambda: krex.check(y16, x16, 1e-3, 1e-3, out=out, sync=False)), x16.numel() * 4)
+    rec("check f8xf8 268M", t_ms(lambda: krex.check(y8, x8, 0.125, 0.125, out=out, sync=False)), x8.numel() * 2)
+    rec("check f32xf32 67M", t_ms(lambda: krex.check(yf, xf, 1e-4, 1e-5, out=out, sync=False)), xf.numel() * 8)
+    rec("flush 1GiB", t_ms(lambda: krex.flush(fl, 1)), GIB)
+    return {"metric": "per-kernel throughput (algorithmic bytes / event time)", "unit": "GB/s",
+            "peak_GBps": HBM_PEAK_GBPS, "kernels": res}
+
+
+def run_copy_calibration():
+    """A plain device-to-device copy of 1 GiB, three times: the kernel whose
+    rocprofv3 FETCH_SIZE / WRITE_SIZE readings calibrate the byte counters."""
+    import torch
+    src = torch.ones(GIB // 4, dtype=torch.int32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -220,7 +293,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--fidelity", action="store_true")
-    ap.add_argument("--samples", type=int, default=300)
+    ap.add_argument("--samples", type=int, default=None)
+    ap.add_argument("--kernels", action="store_true")
+    ap.add_argument("--calib-copy", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (use --gpus 1)", file=sys.stderr)
@@ -229,7 +304,12 @@ def main():
         from paper_2609_30057_amd import fidelity
         print(json.dumps(fidelity.run(samples=args.samples)), flush=True)
         return
+    if args.kernels:
+        print(json.dumps(run_kernels()), flush=True)
+        return
     out = run_gemm_large(args.steps, args.warmup, not args.no_cpu_baseline)
+    if args.calib_copy:
+        run_copy_calibration()
     print(json.dumps(out), flush=True)
 
 

@@ -145,7 +145,7 @@ krex_status krex_inject(void *y, const void *x, int32_t dtype, uint64_t n, uint6
  * need to clear it). Per element, both sides are upcast to fp32 (exact):
  * NaN on either side -> mismatch, counted in nan_count, left out of the
  * maxima; a == b -> close, d = 0, rel = 0; else an infinity on either side
- * -> mismatch, d = rel = +inf; else d = |a - b|, close iff
+ * -> mismatch, d = rel = +inf; else d = |a - b|, close iff d is finite and
  * d <= atol + rtol |b| (fp32, two roundings), rel = d / |b|. The check of a
  * benchmarking command (Section 1; Section 2.1). rtol, atol finite >= 0;
  * n < 2^33; a and b aligned to their element sizes. n = 0 writes the empty
@@ -223,7 +223,8 @@ krex_status krex_fixture_sgemm(uint32_t M, uint32_t N, uint32_t K, const float *
                                void *stream);
 void krex_sgemm_launch(void *user /* krex_sgemm_args* */, void *stream);
 
-/* --- introspection ----------------------------------------------------------- */
+/* --- introspection -------------------------------------------------------------
+ * Counters of this process since its last krex_attach. */
 typedef struct krex_gate_stats {
     uint64_t regions;          /* regions entered by this process */
     uint64_t last_drain_ns;    /* gate closed -> siblings drained, last entry */

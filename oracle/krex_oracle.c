@@ -44,8 +44,8 @@
  *            either side is a mismatch counted in nan_count and left out of
  *            the maxima; equal values are close with d = 0, rel = 0; else an
  *            infinity on either side is a mismatch with d = rel = +inf; else
- *            d = |A - B|, close iff d <= atol + rtol * |B| (two roundings),
- *            rel = d / |B|. Reported: mismatch count, NaN count, max d with
+ *            d = |A - B|, close iff d is finite and d <= atol + rtol * |B|
+ *            (two roundings), rel = d / |B|. Reported: mismatch count, NaN count, max d with
  *            the lowest index attaining it, max rel.
  *   inject   mask_i = [W_mseed[moff + i] < floor(rate * 2^32)]; ROUND mode
  *            y = cvt(x + delta); EXACT mode perturbs by exactly +delta, else
@@ -150,9 +150,12 @@ void ko_words(uint32_t *dst, uint64_t n, uint64_t seed, uint64_t offset)
 
 /* ------------------------------------------------------------------------
  * Conversions. Narrowing is round-to-nearest-even with subnormals kept.
- * NaN inputs give the format's canonical quiet NaN (bf16 0x7FC0, fp16
- * 0x7E00); fp8-e4m3fn has no infinity, so NaN, infinity and any value whose
- * rounded magnitude would exceed 448 give 0x7F with the input's sign.
+ * A NaN input gives the format's one canonical NaN (bf16 0x7FC0, fp16
+ * 0x7E00, fp8 0x7F), whatever its sign and payload: IEEE-754 does not fix
+ * the sign or payload a NaN keeps through arithmetic, so only a canonical
+ * encoding makes a NaN result reproducible across machines. fp8-e4m3fn has
+ * no infinity: infinity and any value whose rounded magnitude would exceed
+ * 448 give 0x7F with the input's sign.
  * ---------------------------------------------------------------------- */
 uint16_t ko_f32_to_bf16(float f)
 {
@@ -208,7 +211,9 @@ uint8_t ko_f32_to_f8e4m3(float f)
     uint32_t x = f2u(f);
     uint8_t sign = (uint8_t)((x >> 24) & 0x80u);
     uint32_t ax = x & 0x7FFFFFFFu;
-    if (ax > 0x43E80000u)           /* NaN, inf, or > 464: rounds to 480+ */
+    if (ax > 0x7F800000u)           /* NaN: the canonical NaN */
+        return 0x7Fu;
+    if (ax > 0x43E80000u)           /* inf, or > 464: rounds to 480+ */
         return (uint8_t)(sign | 0x7Fu);
     if (ax >= 0x3C800000u) {        /* >= 2^-6: a normal e4m3 value */
         uint32_t lsb = (ax >> 20) & 1u;
@@ -612,7 +617,7 @@ int ko_check(const void *a, int dta, const void *b, int dtb, uint64_t n,
             float absb = fabsf(B);
             float rt = rtol * absb;
             float thr = atol + rt;
-            if (!(d <= thr))
+            if (!(d <= thr) || isinf(d))   /* an overflowed difference is never close */
                 r.mismatches++;
             rel = d / absb;
         }

@@ -18,6 +18,7 @@
 #include <chrono>
 #include <condition_variable>
 #include <deque>
+#include <map>
 #include <mutex>
 #include <thread>
 #include <vector>
@@ -219,6 +220,29 @@ krex_status timing_events(int dev, size_t count, hipEvent_t **out)
     return KREX_OK;
 }
 
+// Per-(device, stream) scratch of the check's block partials, allocated on
+// first use and kept: calls on one stream are ordered by the stream, calls
+// on different streams use different buffers.
+std::mutex g_scratch_mu;
+std::map<std::pair<int, hipStream_t>, void *> g_scratch;
+
+krex_status check_scratch(hipStream_t s, void **out)
+{
+    const int dev = current_device();
+    std::lock_guard<std::mutex> g(g_scratch_mu);
+    auto it = g_scratch.find({dev, s});
+    if (it != g_scratch.end()) {
+        *out = it->second;
+        return KREX_OK;
+    }
+    void *p = nullptr;
+    const hipError_t e = hipMalloc(&p, krex::check_scratch_bytes());
+    if (e != hipSuccess) return hip_fail(e);
+    g_scratch[{dev, s}] = p;
+    *out = p;
+    return KREX_OK;
+}
+
 bool finite_f(float x) { return isfinite(x) != 0; }
 
 bool gen_params_ok(int32_t dist, float p0, float p1)
@@ -342,7 +366,10 @@ krex_status krex_check(const void *a, int32_t dta, const void *b, int32_t dtb, u
     if (n > 0 && (!a || !b)) return KREX_EINVAL;
     if (!aligned(a, sa) || !aligned(b, sb) || !aligned(out, 8)) return KREX_EALIGN;
     hipStream_t s = (hipStream_t)stream;
-    return submit(s, [&] { return krex::launch_check(a, dta, b, dtb, n, rtol, atol, out, s); });
+    void *scratch = nullptr;
+    const krex_status rc = check_scratch(s, &scratch);
+    if (rc != KREX_OK) return rc;
+    return submit(s, [&] { return krex::launch_check(a, dta, b, dtb, n, rtol, atol, scratch, out, s); });
 }
 
 krex_status krex_flush(void *buf, uint64_t bytes, uint32_t pattern, void *stream)

@@ -304,6 +304,12 @@ int attach(const char *shm_name, uint32_t flags)
     s.slot = slot;
     s.gated_ = (flags & kNoGate) == 0;
     s.in_region = false;
+    s.regions.store(0);
+    s.last_drain_ns.store(0);
+    s.total_drain_ns.store(0);
+    s.parks.store(0);
+    s.park_ns.store(0);
+    s.recoveries.store(0);
     if (const char *e = getenv("KREX_SPIN_US")) s.spin_us = (uint32_t)strtoul(e, nullptr, 10);
     static bool registered = false;
     if (!registered) {

@@ -8,19 +8,22 @@
 //   k_xform   the same transforms on caller-supplied words.
 //   k_inject  Bernoulli mismatch injection on its own word stream.
 //   k_check   fused allclose check (Section 2.1): 16-byte loads of both
-//             operands, per-thread counters and maxima, wave64 shuffles,
-//             LDS across the block's four waves, one atomic per field per
-//             block, and the last block to finish decodes the packed argmax.
+//             operands, branch-free verdicts, wave64 ballots and shuffles,
+//             LDS across the block's four waves, one partial per block;
+//             k_check_final reduces the partials into the result record.
 //   k_flush   16-byte allocating stores of a pattern (Section 2.1 flush
 //             between iterations; Section 4.2 step 5).
 //   k_probe   fixed-work FMA kernel timed by the fidelity measurement
 //             (Section 6.3, Eq. 1).
 //   k_sgemm   naive fp32 GEMM standing in for a candidate kernel.
 //
-// All loops are grid-stride with a grid sized to the device (a few blocks
-// per CU), so the launch shape never changes a result: every element's
-// value depends only on its index.
+// Work is laid out block-contiguously in address order (block b owns units
+// [b 256 U, (b + 1) 256 U), thread t takes unit b 256 U + u 256 + t), which
+// streams HBM faster on gfx950 than persistent grid-stride loops. The launch
+// shape never changes a result: every element's value depends only on its
+// index.
 #include <hip/hip_runtime.h>
+#include <stdlib.h>
 
 #include <tuple>
 #include <utility>
@@ -48,14 +51,6 @@ static constexpr int kThreads = 256;
 
 template <int DT> struct group_of { static constexpr int G = 4 / dtype_traits<DT>::size; };
 
-static uint32_t grid_for(uint64_t units, int blocks_per_cu)
-{
-    const uint64_t need = (units + kThreads - 1) / kThreads;
-    const uint64_t cap = (uint64_t)device_cus() * (uint64_t)blocks_per_cu;
-    uint64_t g = need < cap ? need : cap;
-    return (uint32_t)(g == 0 ? 1 : g);
-}
-
 // ------------------------------------------------------------------ generation
 
 struct GenParams {
@@ -66,6 +61,7 @@ struct GenParams {
     float p0, p1;      // uniform: lo and fl(hi - lo); normal: mean and std
     uint64_t b0;       // first Philox block
     uint64_t ngroups;  // groups of G blocks
+    uint32_t U;        // groups per thread, block-contiguous
     int vec;           // offset % 4 == 0 and dst 16-byte aligned
 };
 
@@ -75,8 +71,9 @@ __global__ __launch_bounds__(kThreads) void k_gen(GenParams P)
     using T = typename dtype_traits<DT>::storage;
     constexpr int ES = dtype_traits<DT>::size;
     constexpr int G = group_of<DT>::G;
-    const uint64_t stride = (uint64_t)gridDim.x * kThreads;
-    for (uint64_t g = (uint64_t)blockIdx.x * kThreads + threadIdx.x; g < P.ngroups; g += stride) {
+    for (uint32_t u = 0; u < P.U; ++u) {
+        const uint64_t g = ((uint64_t)blockIdx.x * P.U + u) * kThreads + threadIdx.x;
+        if (g >= P.ngroups) break;
         const uint64_t bfirst = P.b0 + g * G;
         union {
             uint4 v;
@@ -92,7 +89,7 @@ __global__ __launch_bounds__(kThreads) void k_gen(GenParams P)
                 float v[4];
                 transform4<DIST>(w, P.p0, P.p1, v);
 #pragma unroll
-                for (int l = 0; l < 4; ++l) pk.s[4 * i + l] = narrow<DT>(v[l]);
+                for (int l = 0; l < 4; ++l) pk.s[4 * i + l] = narrow<DT, DIST == BITCAST>(v[l]);
             }
         }
         const uint64_t j0 = 4 * bfirst - P.offset;
@@ -108,10 +105,34 @@ __global__ __launch_bounds__(kThreads) void k_gen(GenParams P)
     }
 }
 
-template <int DT, int DIST>
-static hipError_t gen_dt_dist(const GenParams &P, hipStream_t s)
+// Units per thread and grid of the block-contiguous layout: block b owns
+// units [b 256 U, (b + 1) 256 U). One unit per thread (a one-shot grid in
+// address order) streams HBM fastest on gfx950; U grows only to keep a
+// dispatch within 2^31 work-items.
+static void shape(uint64_t units, uint32_t u_pref, uint32_t *U, uint32_t *grid)
 {
-    const uint32_t grid = grid_for(P.ngroups, 8);
+    uint64_t u = u_pref ? u_pref : 1;
+    const uint64_t min_u = (units + (1ull << 31) - 1) >> 31;
+    if (u < min_u) u = min_u;
+    uint64_t g = (units + kThreads * u - 1) / (kThreads * u);
+    *U = (uint32_t)u;
+    *grid = (uint32_t)(g ? g : 1);
+}
+
+static uint32_t tune_env(const char *name, uint32_t dflt)
+{
+    const char *e = getenv(name);
+    if (!e) return dflt;
+    const unsigned long v = strtoul(e, nullptr, 10);
+    return v ? (uint32_t)v : dflt;
+}
+
+template <int DT, int DIST>
+static hipError_t gen_dt_dist(GenParams P, hipStream_t s)
+{
+    static const uint32_t u_pref = tune_env("KREX_GEN_U", 1);
+    uint32_t grid;
+    shape(P.ngroups, u_pref, &P.U, &grid);
     return launch(k_gen<DT, DIST>, dim3(grid), dim3(kThreads), s, P);
 }
 
@@ -166,6 +187,7 @@ struct XformParams {
     uint64_t n;
     float p0, p1;
     uint64_t ngroups;
+    uint32_t U;
     int vec;
 };
 
@@ -175,8 +197,9 @@ __global__ __launch_bounds__(kThreads) void k_xform(XformParams P)
     using T = typename dtype_traits<DT>::storage;
     constexpr int ES = dtype_traits<DT>::size;
     constexpr int G = group_of<DT>::G;
-    const uint64_t stride = (uint64_t)gridDim.x * kThreads;
-    for (uint64_t g = (uint64_t)blockIdx.x * kThreads + threadIdx.x; g < P.ngroups; g += stride) {
+    for (uint32_t u = 0; u < P.U; ++u) {
+        const uint64_t g = ((uint64_t)blockIdx.x * P.U + u) * kThreads + threadIdx.x;
+        if (g >= P.ngroups) break;
         const uint64_t j0 = g * 4 * G;
         if (P.vec && j0 + 4 * G <= P.n) {
             union {
@@ -195,7 +218,7 @@ __global__ __launch_bounds__(kThreads) void k_xform(XformParams P)
                     float v[4];
                     transform4<DIST>(w, P.p0, P.p1, v);
 #pragma unroll
-                    for (int l = 0; l < 4; ++l) pk.s[4 * i + l] = narrow<DT>(v[l]);
+                    for (int l = 0; l < 4; ++l) pk.s[4 * i + l] = narrow<DT, DIST == BITCAST>(v[l]);
                 }
             }
             *reinterpret_cast<uint4 *>(P.dst + j0 * ES) = pk.v;
@@ -218,7 +241,7 @@ __global__ __launch_bounds__(kThreads) void k_xform(XformParams P)
                     } else {
                         v = __uint_as_float(P.words[j]);
                     }
-                    out = narrow<DT>(v);
+                    out = narrow<DT, DIST == BITCAST>(v);
                 }
                 reinterpret_cast<T *>(P.dst)[j] = out;
             }
@@ -227,9 +250,10 @@ __global__ __launch_bounds__(kThreads) void k_xform(XformParams P)
 }
 
 template <int DT>
-static hipError_t xform_dt(const XformParams &P, int dist, hipStream_t s)
+static hipError_t xform_dt(XformParams P, int dist, hipStream_t s)
 {
-    const uint32_t grid = grid_for(P.ngroups, 8);
+    uint32_t grid;
+    shape(P.ngroups, 1, &P.U, &grid);
     if constexpr (DT == U32) return launch(k_xform<U32, UNIFORM>, dim3(grid), dim3(kThreads), s, P);
     switch (dist) {
     case UNIFORM: return launch(k_xform<DT, UNIFORM>, dim3(grid), dim3(kThreads), s, P);
@@ -272,6 +296,7 @@ struct InjectParams {
     float delta;
     uint64_t b0;
     uint64_t ngroups;
+    uint32_t U;
     int vec;
 };
 
@@ -286,10 +311,10 @@ __device__ __forceinline__ typename dtype_traits<DT>::storage perturb(typename d
     } else {
         const float sp = X + delta;
         const float dp = sp - X;
-        if (dp == delta && widen<DT>(narrow<DT>(sp)) == sp) return narrow<DT>(sp);
+        if (dp == delta && widen<DT>(narrow<DT, false>(sp)) == sp) return narrow<DT, false>(sp);
         const float sm = X - delta;
         const float dm = X - sm;
-        if (dm == delta && widen<DT>(narrow<DT>(sm)) == sm) return narrow<DT>(sm);
+        if (dm == delta && widen<DT>(narrow<DT, false>(sm)) == sm) return narrow<DT, false>(sm);
         return bits;
     }
 }
@@ -300,8 +325,9 @@ __global__ __launch_bounds__(kThreads) void k_inject(InjectParams P)
     using T = typename dtype_traits<DT>::storage;
     constexpr int ES = dtype_traits<DT>::size;
     constexpr int G = group_of<DT>::G;
-    const uint64_t stride = (uint64_t)gridDim.x * kThreads;
-    for (uint64_t g = (uint64_t)blockIdx.x * kThreads + threadIdx.x; g < P.ngroups; g += stride) {
+    for (uint32_t u = 0; u < P.U; ++u) {
+        const uint64_t g = ((uint64_t)blockIdx.x * P.U + u) * kThreads + threadIdx.x;
+        if (g >= P.ngroups) break;
         const uint64_t bfirst = P.b0 + g * G;
         const uint64_t j0 = 4 * bfirst - P.moff;
         if (P.vec && j0 + 4 * G <= P.n) {
@@ -335,9 +361,11 @@ __global__ __launch_bounds__(kThreads) void k_inject(InjectParams P)
 }
 
 template <int DT>
-static hipError_t inject_dt(const InjectParams &P, int mode, hipStream_t s)
+static hipError_t inject_dt(InjectParams P, int mode, hipStream_t s)
 {
-    const uint32_t grid = grid_for(P.ngroups, 8);
+    static const uint32_t u_pref = tune_env("KREX_INJECT_U", 1);
+    uint32_t grid;
+    shape(P.ngroups, u_pref, &P.U, &grid);
     if (mode == INJ_ROUND) return launch(k_inject<DT, INJ_ROUND>, dim3(grid), dim3(kThreads), s, P);
     return launch(k_inject<DT, INJ_EXACT>, dim3(grid), dim3(kThreads), s, P);
 }
@@ -370,205 +398,391 @@ hipError_t launch_inject(void *y, const void *x, int dt, uint64_t n, uint64_t ms
 }
 
 // ---------------------------------------------------------------------- check
+//
+// Two launches and no atomics. k_check: block b owns chunks
+// [b 256 U, (b + 1) 256 U) of E elements (one 16-byte vector of the
+// narrower operand); thread t takes chunk b 256 U + u 256 + t for u < U, so
+// every step of a wave reads contiguous memory. Per element the verdict is
+// branch-free; mismatch and NaN counts are wave ballots summed on the scalar
+// unit; the per-lane maximum |a - b| is tracked per chunk and its first index
+// recovered at the end by re-reading that one chunk. Each block writes one
+// 32-byte partial with plain stores; k_check_final reduces the partials and
+// writes the result record.
+//
+// max_rel without a division per element: a lane keeps the pair (d*, b*)
+// with the largest exact ratio d / |b| among its elements with finite
+// positive d, comparing d b* > d* |b| in fp64, where the products of two
+// fp32 values are exact. One correctly rounded fp32 division per lane then
+// gives fl(max d / |b|), which equals max fl(d / |b|) because rounding is
+// monotone. Infinite d (an infinite operand, or overflow) enters as the pair
+// (inf, 0), ratio +inf.
+//
+// (A per-block atomic finish costs ~12 ns per same-address device atomic on
+// this GPU, serialised: 2048 blocks x 5 atomics is ~130 us, longer than
+// reading 100 MB.)
 
 static constexpr uint64_t kIdxMask = (1ull << 33) - 1;   // n < 2^33
+static constexpr int kMaxCheckBlocks = 4096;
+static constexpr int kFinalThreads = 1024;
 
-struct CheckAcc {
-    uint32_t mism;
-    uint32_t nan;
-    uint64_t key;     // (bits(d) << 33) | (kIdxMask - i): max = largest d, lowest i
-    float rel;
+struct CheckPartial {
+    uint64_t mism;
+    uint64_t nan;
+    uint64_t key;       // (bits(max d) << 33) | (kIdxMask - index); 0 = no NaN-free element
+    uint32_t rel_bits;  // max rel (non-negative fp32 bits)
+    uint32_t pad;
 };
 
-__device__ __forceinline__ void check_one(float A, float B, uint64_t i, float rtol, float atol, CheckAcc &acc)
+static_assert(sizeof(CheckPartial) == 32, "partial layout");
+
+size_t check_scratch_bytes() { return (size_t)kMaxCheckBlocks * sizeof(CheckPartial); }
+
+struct LaneAcc {
+    uint32_t wmism, wnan;   // wave totals (exact in the wave's first lane)
+    float rd, rb;           // element with the largest ratio d / |b| (rb = 0: +inf)
+};
+
+__device__ __forceinline__ uint32_t popc(uint64_t m) { return (uint32_t)__builtin_popcountll(m); }
+
+// One element: counts, ratio candidate; returns d (0 when equal, NaN when
+// unordered) for the |a - b| maximum.
+__device__ __forceinline__ float check_elem(float A, float B, float rtol, float atol, LaneAcc &acc)
 {
-    if (A != A || B != B) {
-        acc.mism += 1u;
-        acc.nan += 1u;
-        return;
-    }
-    float d, r;
-    if (A == B) {
-        d = 0.0f;
-        r = 0.0f;
-    } else if (__builtin_fabsf(A) == __builtin_inff() || __builtin_fabsf(B) == __builtin_inff()) {
-        acc.mism += 1u;
-        d = __builtin_inff();
-        r = __builtin_inff();
-    } else {
-        const float diff = A - B;
-        d = __builtin_fabsf(diff);
-        const float ab = __builtin_fabsf(B);
-        const float rt = rtol * ab;
-        const float thr = atol + rt;
-        acc.mism += (d <= thr) ? 0u : 1u;
-        r = d / ab;
-    }
-    const uint64_t k = ((uint64_t)__float_as_uint(d) << 33) | (kIdxMask - i);
-    acc.key = k > acc.key ? k : acc.key;
-    acc.rel = r > acc.rel ? r : acc.rel;
+    const float d0 = __builtin_fabsf(A - B);
+    const float ab = __builtin_fabsf(B);
+    const bool unord = __builtin_isunordered(A, B);
+    const bool eq = (A == B);
+    // d0 is +inf exactly when the operands differ and one is infinite, or
+    // their difference overflows: never close, ratio +inf.
+    const bool dinf = d0 == __builtin_inff();
+    const float rt = rtol * ab;
+    const float thr = atol + rt;
+    // Non-short-circuit operators keep every predicate a lane mask (no branch).
+    const bool close = eq | ((d0 <= thr) & !dinf);
+    acc.wmism += popc(__ballot(!close));
+    acc.wnan += popc(__ballot(unord));
+    // Ratio candidate (d0, bn); an infinite d0 enters as (inf, 0), ratio +inf,
+    // which no later pair exceeds. d0 = 0 and NaN never compare greater.
+    const float bn = dinf ? 0.0f : ab;
+    const bool greater = (double)d0 * (double)acc.rb > (double)acc.rd * (double)bn;
+    acc.rd = greater ? d0 : acc.rd;
+    acc.rb = greater ? bn : acc.rb;
+    return eq ? 0.0f : d0;
 }
 
-template <int DA, int DB>
-__global__ __launch_bounds__(kThreads) void k_check(const uint8_t *a, const uint8_t *b, uint64_t n, float rtol,
-                                                    float atol, krex_check_result *out, int vec)
+// The same d, for re-reading the best chunk.
+__device__ __forceinline__ float elem_d(float A, float B)
 {
+    return (A == B) ? 0.0f : __builtin_fabsf(A - B);
+}
+
+template <int DA, int DB, bool VEC>
+struct ChunkIO {
     using TA = typename dtype_traits<DA>::storage;
     using TB = typename dtype_traits<DB>::storage;
-    constexpr int SA = dtype_traits<DA>::size;
-    constexpr int SB = dtype_traits<DB>::size;
-    constexpr int E = 16 / (SA < SB ? SA : SB);      // elements per chunk
-    constexpr int VA = E * SA / 16;                  // 16-byte vectors of a per chunk
-    constexpr int VB = E * SB / 16;
-    CheckAcc acc{0u, 0u, 0ull, 0.0f};
-    const uint64_t tid = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
-    const uint64_t stride = (uint64_t)gridDim.x * kThreads;
-    const uint64_t nchunks = vec ? n / E : 0;
-    for (uint64_t c = tid; c < nchunks; c += stride) {
+    static constexpr int SA = dtype_traits<DA>::size;
+    static constexpr int SB = dtype_traits<DB>::size;
+    static constexpr int E = 16 / (SA < SB ? SA : SB);
+    static constexpr int VA = E * SA / 16;
+    static constexpr int VB = E * SB / 16;
+
+    // Raw bytes of one chunk: 16-byte vectors of each operand.
+    struct Raw {
         union {
             uint4 v[VA];
             TA s[E];
-        } ua;
+        } a;
         union {
             uint4 v[VB];
             TB s[E];
-        } ub;
-#pragma unroll
-        for (int i = 0; i < VA; ++i) ua.v[i] = reinterpret_cast<const uint4 *>(a)[c * VA + i];
-#pragma unroll
-        for (int i = 0; i < VB; ++i) ub.v[i] = reinterpret_cast<const uint4 *>(b)[c * VB + i];
-#pragma unroll
-        for (int e = 0; e < E; ++e)
-            check_one(widen<DA>(ua.s[e]), widen<DB>(ub.s[e]), c * E + e, rtol, atol, acc);
-    }
-    for (uint64_t i = nchunks * E + tid; i < n; i += stride)
-        check_one(widen<DA>(reinterpret_cast<const TA *>(a)[i]), widen<DB>(reinterpret_cast<const TB *>(b)[i]), i,
-                  rtol, atol, acc);
+        } b;
+    };
 
-    // wave64 reduction
+    __device__ __forceinline__ static void load_raw(const uint8_t *a, const uint8_t *b, uint64_t c, Raw &r)
+    {
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-        acc.mism += __shfl_xor(acc.mism, off, 64);
-        acc.nan += __shfl_xor(acc.nan, off, 64);
-        const uint64_t k = __shfl_xor((unsigned long long)acc.key, off, 64);
-        acc.key = k > acc.key ? k : acc.key;
-        const float r = __shfl_xor(acc.rel, off, 64);
-        acc.rel = r > acc.rel ? r : acc.rel;
-    }
-    __shared__ uint32_t s_mism[kThreads / 64], s_nan[kThreads / 64];
-    __shared__ uint64_t s_key[kThreads / 64];
-    __shared__ float s_rel[kThreads / 64];
-    const int wave = threadIdx.x / 64;
-    if ((threadIdx.x & 63) == 0) {
-        s_mism[wave] = acc.mism;
-        s_nan[wave] = acc.nan;
-        s_key[wave] = acc.key;
-        s_rel[wave] = acc.rel;
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        uint64_t m = 0, nn = 0, key = 0;
-        float rel = 0.0f;
+        for (int i = 0; i < VA; ++i) r.a.v[i] = reinterpret_cast<const uint4 *>(a)[c * VA + i];
 #pragma unroll
-        for (int w = 0; w < kThreads / 64; ++w) {
-            m += s_mism[w];
-            nn += s_nan[w];
-            key = s_key[w] > key ? s_key[w] : key;
-            rel = s_rel[w] > rel ? s_rel[w] : rel;
+        for (int i = 0; i < VB; ++i) r.b.v[i] = reinterpret_cast<const uint4 *>(b)[c * VB + i];
+    }
+
+    __device__ __forceinline__ static void widen_raw(const Raw &r, float (&A)[E], float (&B)[E])
+    {
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            A[e] = widen<DA>(r.a.s[e]);
+            B[e] = widen<DB>(r.b.s[e]);
         }
-        if (m) atomicAdd((unsigned long long *)&out->mismatches, (unsigned long long)m);
-        if (nn) atomicAdd((unsigned long long *)&out->nan_count, (unsigned long long)nn);
-        if (key) atomicMax((unsigned long long *)&out->reserved[0], (unsigned long long)key);
-        if (rel > 0.0f) atomicMax((unsigned int *)&out->max_rel, __float_as_uint(rel));
-        __threadfence();
-        const unsigned int ticket = atomicAdd((unsigned int *)&out->reserved[1], 1u);
-        if (ticket == gridDim.x - 1) {
-            __threadfence();
-            const uint64_t K = __hip_atomic_load(&out->reserved[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if (K == 0) {
-                out->argmax_abs = ~0ull;
-                out->max_abs = 0.0f;
-            } else {
-                out->max_abs = __uint_as_float((uint32_t)(K >> 33));
-                out->argmax_abs = kIdxMask - (K & kIdxMask);
+    }
+
+    __device__ __forceinline__ static void load(const uint8_t *a, const uint8_t *b, uint64_t c, float (&A)[E],
+                                                float (&B)[E])
+    {
+        if constexpr (VEC) {
+            Raw r;
+            load_raw(a, b, c, r);
+            widen_raw(r, A, B);
+        } else {
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                A[e] = widen<DA>(reinterpret_cast<const TA *>(a)[c * E + e]);
+                B[e] = widen<DB>(reinterpret_cast<const TB *>(b)[c * E + e]);
             }
         }
     }
+};
+
+template <int DA, int DB, bool VEC>
+__global__ __launch_bounds__(kThreads) void k_check(const uint8_t *a, const uint8_t *b, uint64_t n, float rtol,
+                                                    float atol, CheckPartial *partials, uint32_t U)
+{
+    using IO = ChunkIO<DA, DB, VEC>;
+    constexpr int E = IO::E;
+    const uint32_t t = threadIdx.x;
+    const uint64_t nchunks = n / E;
+    const uint64_t base = (uint64_t)blockIdx.x * kThreads * U;
+    LaneAcc acc{0u, 0u, 0.0f, 1.0f};
+    float best_d = -1.0f;               // largest non-NaN d seen by this lane
+    uint32_t best_c = 0;                // its chunk
+    auto process = [&](const float (&A)[E], const float (&B)[E], uint64_t c) {
+        float cmax = -1.0f;   // NaN d (unordered) is ignored by the maximum
+#pragma unroll
+        for (int e = 0; e < E; ++e) cmax = __builtin_fmaxf(cmax, check_elem(A[e], B[e], rtol, atol, acc));
+        if (cmax > best_d) {
+            best_d = cmax;
+            best_c = (uint32_t)c;
+        }
+    };
+    if constexpr (VEC) {
+        // Software pipeline: the next chunk's loads are in flight while the
+        // current one is evaluated. A lane's chunks only grow with u, so the
+        // first lane of a wave is active whenever any lane is.
+        typename IO::Raw cur, nxt;
+        uint64_t c = base + t;
+        bool have = c < nchunks;
+        if (have) IO::load_raw(a, b, c, cur);
+        for (uint32_t u = 0; u < U; ++u) {
+            const uint64_t cn = c + kThreads;
+            const bool have_n = (u + 1 < U) && cn < nchunks;
+            if (have_n) IO::load_raw(a, b, cn, nxt);
+            if (have) {
+                float A[E], B[E];
+                IO::widen_raw(cur, A, B);
+                process(A, B, c);
+            }
+            cur = nxt;
+            c = cn;
+            have = have_n;
+        }
+    } else {
+        for (uint32_t u = 0; u < U; ++u) {
+            const uint64_t c = base + (uint64_t)u * kThreads + t;
+            if (c < nchunks) {
+                float A[E], B[E];
+                IO::load(a, b, c, A, B);
+                process(A, B, c);
+            }
+        }
+    }
+    // First element of the lane's best chunk attaining best_d.
+    uint64_t best_i = ~0ull;
+    if (best_d >= 0.0f) {
+        float A[E], B[E];
+        IO::load(a, b, best_c, A, B);
+        for (int e = E - 1; e >= 0; --e)
+            if (elem_d(A[e], B[e]) == best_d) best_i = (uint64_t)best_c * E + e;
+    }
+    // The n mod E tail: the first block's first lanes, one element each.
+    const uint64_t tail0 = nchunks * E;
+    if (blockIdx.x == 0 && tail0 + t < n) {
+        const uint64_t i = tail0 + t;
+        const float A = widen<DA>(reinterpret_cast<const typename IO::TA *>(a)[i]);
+        const float B = widen<DB>(reinterpret_cast<const typename IO::TB *>(b)[i]);
+        const float d = check_elem(A, B, rtol, atol, acc);
+        if (d > best_d) {     // tail indices exceed every chunk index
+            best_d = d;
+            best_i = i;
+        }
+    }
+    float rel = acc.rd / acc.rb;                 // +inf when rb = 0 < rd; 0 for the initial (0, 1)
+    uint64_t key = best_d >= 0.0f ? (((uint64_t)__float_as_uint(best_d) << 33) | (kIdxMask - best_i)) : 0ull;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const uint64_t k2 = __shfl_xor((unsigned long long)key, off, 64);
+        key = k2 > key ? k2 : key;
+        const float r2 = __shfl_xor(rel, off, 64);
+        rel = r2 > rel ? r2 : rel;
+    }
+    const uint32_t wm = __shfl(acc.wmism, 0, 64), wn = __shfl(acc.wnan, 0, 64);
+    __shared__ uint64_t s_key[kThreads / 64];
+    __shared__ uint32_t s_m[kThreads / 64], s_n[kThreads / 64];
+    __shared__ float s_r[kThreads / 64];
+    const int w = t / 64;
+    if ((t & 63) == 0) {
+        s_key[w] = key;
+        s_m[w] = wm;
+        s_n[w] = wn;
+        s_r[w] = rel;
+    }
+    __syncthreads();
+    if (t == 0) {
+        CheckPartial p;
+        p.mism = 0;
+        p.nan = 0;
+        p.key = 0;
+        float r = 0.0f;
+#pragma unroll
+        for (int i = 0; i < kThreads / 64; ++i) {
+            p.mism += s_m[i];
+            p.nan += s_n[i];
+            p.key = s_key[i] > p.key ? s_key[i] : p.key;
+            r = s_r[i] > r ? s_r[i] : r;
+        }
+        p.rel_bits = __float_as_uint(r);
+        p.pad = 0;
+        partials[blockIdx.x] = p;
+    }
 }
 
-__global__ void k_check_init(krex_check_result *out, uint64_t n)
+__global__ __launch_bounds__(kFinalThreads) void k_check_final(const CheckPartial *partials, uint32_t nblocks,
+                                                               uint64_t n, krex_check_result *out)
 {
-    out->n = n;
-    out->mismatches = 0;
-    out->nan_count = 0;
-    out->argmax_abs = ~0ull;
-    out->max_abs = 0.0f;
-    out->max_rel = 0.0f;
-    out->reserved[0] = 0;
-    out->reserved[1] = 0;
-    out->reserved[2] = 0;
+    constexpr int PER = kMaxCheckBlocks / kFinalThreads;
+    uint64_t m = 0, nn = 0, key = 0;
+    uint32_t rb = 0;
+    CheckPartial p[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const uint32_t i = threadIdx.x + (uint32_t)j * kFinalThreads;
+        if (i < nblocks) p[j] = partials[i];
+        else p[j] = CheckPartial{0, 0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        m += p[j].mism;
+        nn += p[j].nan;
+        key = p[j].key > key ? p[j].key : key;
+        rb = p[j].rel_bits > rb ? p[j].rel_bits : rb;   // non-negative floats order as integers
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        m += __shfl_xor((unsigned long long)m, off, 64);
+        nn += __shfl_xor((unsigned long long)nn, off, 64);
+        const uint64_t k2 = __shfl_xor((unsigned long long)key, off, 64);
+        key = k2 > key ? k2 : key;
+        const uint32_t r2 = __shfl_xor(rb, off, 64);
+        rb = r2 > rb ? r2 : rb;
+    }
+    __shared__ uint64_t s_m[kFinalThreads / 64], s_n[kFinalThreads / 64], s_k[kFinalThreads / 64];
+    __shared__ uint32_t s_r[kFinalThreads / 64];
+    const int w = threadIdx.x / 64;
+    if ((threadIdx.x & 63) == 0) {
+        s_m[w] = m;
+        s_n[w] = nn;
+        s_k[w] = key;
+        s_r[w] = rb;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int i = 1; i < kFinalThreads / 64; ++i) {
+            s_m[0] += s_m[i];
+            s_n[0] += s_n[i];
+            s_k[0] = s_k[i] > s_k[0] ? s_k[i] : s_k[0];
+            s_r[0] = s_r[i] > s_r[0] ? s_r[i] : s_r[0];
+        }
+        const uint64_t K = s_k[0];
+        out->n = n;
+        out->mismatches = s_m[0];
+        out->nan_count = s_n[0];
+        out->argmax_abs = K ? kIdxMask - (K & kIdxMask) : ~0ull;
+        out->max_abs = K ? __uint_as_float((uint32_t)(K >> 33)) : 0.0f;
+        out->max_rel = __uint_as_float(s_r[0]);
+        out->reserved[0] = 0;
+        out->reserved[1] = 0;
+        out->reserved[2] = 0;
+    }
 }
 
 template <int DA, int DB>
-static hipError_t check_ab(const void *a, const void *b, uint64_t n, float rtol, float atol, krex_check_result *out,
-                           hipStream_t s)
+static hipError_t check_ab(const void *a, const void *b, uint64_t n, float rtol, float atol, void *scratch,
+                           krex_check_result *out, hipStream_t s)
 {
     constexpr int SA = dtype_traits<DA>::size, SB = dtype_traits<DB>::size;
     constexpr int E = 16 / (SA < SB ? SA : SB);
-    const int vec = (((uintptr_t)a & 15u) == 0 && ((uintptr_t)b & 15u) == 0) ? 1 : 0;
-    const uint64_t units = vec ? (n / E > 0 ? n / E : 1) : n;
-    const uint32_t grid = grid_for(units, 8);
-    return launch(k_check<DA, DB>, dim3(grid), dim3(kThreads), s, (const uint8_t *)a, (const uint8_t *)b, n, rtol,
-                  atol, out, vec);
+    const bool vec = (((uintptr_t)a & 15u) == 0 && ((uintptr_t)b & 15u) == 0);
+    const uint64_t nchunks = n / E;
+    // Chunks per thread: enough that the grid stays within the partial
+    // buffer, at least the tuning floor.
+    static const uint32_t u_floor = tune_env("KREX_CHECK_U", 1);
+    uint64_t U = (nchunks + (uint64_t)kThreads * kMaxCheckBlocks - 1) / ((uint64_t)kThreads * kMaxCheckBlocks);
+    if (U < u_floor) U = u_floor;
+    if (U == 0) U = 1;
+    uint64_t G = (nchunks + (uint64_t)kThreads * U - 1) / ((uint64_t)kThreads * U);
+    if (G == 0) G = 1;   // the tail alone
+    CheckPartial *parts = (CheckPartial *)scratch;
+    hipError_t e;
+    if (vec)
+        e = launch(k_check<DA, DB, true>, dim3((uint32_t)G), dim3(kThreads), s, (const uint8_t *)a, (const uint8_t *)b,
+                   n, rtol, atol, parts, (uint32_t)U);
+    else
+        e = launch(k_check<DA, DB, false>, dim3((uint32_t)G), dim3(kThreads), s, (const uint8_t *)a,
+                   (const uint8_t *)b, n, rtol, atol, parts, (uint32_t)U);
+    if (e != hipSuccess) return e;
+    return launch(k_check_final, dim3(1), dim3(kFinalThreads), s, (const CheckPartial *)parts, (uint32_t)G, n, out);
 }
 
 template <int DA>
-static hipError_t check_a(const void *a, int dtb, const void *b, uint64_t n, float rtol, float atol,
+static hipError_t check_a(const void *a, int dtb, const void *b, uint64_t n, float rtol, float atol, void *scratch,
                           krex_check_result *out, hipStream_t s)
 {
     switch (dtb) {
-    case F32: return check_ab<DA, F32>(a, b, n, rtol, atol, out, s);
-    case BF16: return check_ab<DA, BF16>(a, b, n, rtol, atol, out, s);
-    case F16: return check_ab<DA, F16>(a, b, n, rtol, atol, out, s);
-    default: return check_ab<DA, F8>(a, b, n, rtol, atol, out, s);
+    case F32: return check_ab<DA, F32>(a, b, n, rtol, atol, scratch, out, s);
+    case BF16: return check_ab<DA, BF16>(a, b, n, rtol, atol, scratch, out, s);
+    case F16: return check_ab<DA, F16>(a, b, n, rtol, atol, scratch, out, s);
+    default: return check_ab<DA, F8>(a, b, n, rtol, atol, scratch, out, s);
     }
 }
 
 hipError_t launch_check(const void *a, int dta, const void *b, int dtb, uint64_t n, float rtol, float atol,
-                        krex_check_result *out, hipStream_t s)
+                        void *scratch, krex_check_result *out, hipStream_t s)
 {
-    hipError_t e = launch(k_check_init, dim3(1), dim3(1), s, out, n);
-    if (e != hipSuccess || n == 0) return e;
+    if (n == 0)
+        return launch(k_check_final, dim3(1), dim3(kFinalThreads), s, (const CheckPartial *)scratch, 0u, n, out);
     switch (dta) {
-    case F32: return check_a<F32>(a, dtb, b, n, rtol, atol, out, s);
-    case BF16: return check_a<BF16>(a, dtb, b, n, rtol, atol, out, s);
-    case F16: return check_a<F16>(a, dtb, b, n, rtol, atol, out, s);
-    default: return check_a<F8>(a, dtb, b, n, rtol, atol, out, s);
+    case F32: return check_a<F32>(a, dtb, b, n, rtol, atol, scratch, out, s);
+    case BF16: return check_a<BF16>(a, dtb, b, n, rtol, atol, scratch, out, s);
+    case F16: return check_a<F16>(a, dtb, b, n, rtol, atol, scratch, out, s);
+    default: return check_a<F8>(a, dtb, b, n, rtol, atol, scratch, out, s);
     }
 }
 
 // ---------------------------------------------------------------------- flush
 
+// One 16-byte store per thread, blocks in address order. On gfx950 this
+// dispatch-ordered shape streams writes at ~85% of HBM peak, well above
+// persistent grid-stride loops (whose 2048 concurrently active blocks spread
+// each wave of stores across the whole buffer).
 __global__ __launch_bounds__(kThreads) void k_flush(uint4 *buf, uint64_t nvec, uint32_t pattern)
 {
-    const uint4 v = make_uint4(pattern, pattern, pattern, pattern);
-    const uint64_t stride = (uint64_t)gridDim.x * kThreads;
-    uint64_t i = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
-    for (; i + 3 * stride < nvec; i += 4 * stride) {
-        buf[i] = v;
-        buf[i + stride] = v;
-        buf[i + 2 * stride] = v;
-        buf[i + 3 * stride] = v;
-    }
-    for (; i < nvec; i += stride) buf[i] = v;
+    const uint64_t i = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i < nvec) buf[i] = make_uint4(pattern, pattern, pattern, pattern);
 }
 
 hipError_t launch_flush(void *buf, uint64_t bytes, uint32_t pattern, hipStream_t s)
 {
-    const uint64_t nvec = bytes / 16;
-    if (nvec == 0) return hipSuccess;
-    const uint32_t grid = grid_for(nvec, 8);
-    return launch(k_flush, dim3(grid), dim3(kThreads), s, (uint4 *)buf, nvec, pattern);
+    // A dispatch covers at most 2^32 - 1 work-items; split larger buffers.
+    const uint64_t per_launch = (1ull << 31);   // vectors (32 GiB) per dispatch
+    uint4 *p = (uint4 *)buf;
+    uint64_t nvec = bytes / 16;
+    while (nvec > 0) {
+        const uint64_t m = nvec < per_launch ? nvec : per_launch;
+        const uint32_t grid = (uint32_t)((m + kThreads - 1) / kThreads);
+        const hipError_t e = launch(k_flush, dim3(grid), dim3(kThreads), s, p, m, pattern);
+        if (e != hipSuccess) return e;
+        p += m;
+        nvec -= m;
+    }
+    return hipSuccess;
 }
 
 // ---------------------------------------------------------------------- probe

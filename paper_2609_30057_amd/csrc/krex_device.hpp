@@ -106,7 +106,8 @@ __device__ __forceinline__ uint8_t to_f8(float f)
     const uint32_t x = __float_as_uint(f);
     const uint32_t sign = (x >> 24) & 0x80u;
     const uint32_t ax = x & 0x7FFFFFFFu;
-    if (ax > 0x43E80000u) return (uint8_t)(sign | 0x7Fu);               // NaN, inf, > 464
+    if (ax > 0x7F800000u) return 0x7Fu;                                 // NaN: canonical
+    if (ax > 0x43E80000u) return (uint8_t)(sign | 0x7Fu);               // inf, > 464
     if (ax >= 0x3C800000u) {                                            // normal e4m3
         const uint32_t r = ax + 0x7FFFFu + ((ax >> 20) & 1u);
         return (uint8_t)(sign | ((r - (120u << 23)) >> 20));
@@ -144,13 +145,40 @@ __device__ __forceinline__ float from_f8(uint32_t h)
     return __uint_as_float(sign | ((e + 120u) << 23) | (m << 20));
 }
 
-template <int DT>
+// gfx950 conversion instructions (v_cvt_pk_bf16_f32, v_cvt_f16_f32,
+// v_cvt_pk_fp8_f32 without clamp, v_cvt_f32_f16, v_cvt_f32_fp8). Measured
+// against the bit-level definitions above over all 2^32 fp32 inputs and all
+// 2^16 / 2^8 narrow inputs: identical for every input that is not a NaN; a
+// NaN input gives a NaN with another payload or sign. `narrow` therefore
+// uses them directly only where no NaN can reach it and maps NaN to the
+// canonical pattern otherwise. The upcasts' NaN payloads differ too, which
+// no caller observes (a NaN is only tested as a NaN or narrowed again).
+__device__ __forceinline__ uint16_t to_bf16_hw(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+__device__ __forceinline__ uint16_t to_f16_hw(float f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
+__device__ __forceinline__ uint8_t to_f8_hw(float f)
+{
+    return (uint8_t)(__builtin_amdgcn_cvt_pk_fp8_f32(f, 0.0f, 0, false) & 0xFF);
+}
+
+// NAN_IN: whether v may be a NaN.
+template <int DT, bool NAN_IN = true>
 __device__ __forceinline__ typename dtype_traits<DT>::storage narrow(float v)
 {
-    if constexpr (DT == F32) return __float_as_uint(v);
-    else if constexpr (DT == BF16) return to_bf16(v);
-    else if constexpr (DT == F16) return to_f16(v);
-    else return to_f8(v);
+    if constexpr (DT == F32) {
+        return __float_as_uint(v);
+    } else if constexpr (DT == BF16) {
+        const uint16_t h = to_bf16_hw(v);
+        if constexpr (NAN_IN) return (v != v) ? (uint16_t)0x7FC0u : h;
+        return h;
+    } else if constexpr (DT == F16) {
+        const uint16_t h = to_f16_hw(v);
+        if constexpr (NAN_IN) return (v != v) ? (uint16_t)0x7E00u : h;
+        return h;
+    } else {
+        const uint8_t h = to_f8_hw(v);
+        if constexpr (NAN_IN) return (v != v) ? (uint8_t)0x7Fu : h;
+        return h;
+    }
 }
 
 template <int DT>
@@ -158,8 +186,8 @@ __device__ __forceinline__ float widen(uint32_t bits)
 {
     if constexpr (DT == F32) return __uint_as_float(bits);
     else if constexpr (DT == BF16) return from_bf16(bits);
-    else if constexpr (DT == F16) return from_f16(bits);
-    else return from_f8(bits);
+    else if constexpr (DT == F16) return (float)__builtin_bit_cast(_Float16, (uint16_t)bits);
+    else return __builtin_amdgcn_cvt_f32_fp8((int)bits, 0);
 }
 
 // ---------------------------------------------------------------- fp32 math

@@ -20,8 +20,11 @@ hipError_t launch_xform(void *dst, int dt, uint64_t n, const uint32_t *words, in
                         hipStream_t s);
 hipError_t launch_inject(void *y, const void *x, int dt, uint64_t n, uint64_t mseed, uint64_t moff, uint64_t T,
                          float delta, int mode, hipStream_t s);
+// The check reduces per-block partials held in `scratch` (device memory of
+// check_scratch_bytes()); calls that may overlap need distinct scratch.
+size_t check_scratch_bytes();
 hipError_t launch_check(const void *a, int dta, const void *b, int dtb, uint64_t n, float rtol, float atol,
-                        krex_check_result *out, hipStream_t s);
+                        void *scratch, krex_check_result *out, hipStream_t s);
 hipError_t launch_flush(void *buf, uint64_t bytes, uint32_t pattern, hipStream_t s);
 hipError_t launch_probe(uint64_t iters, float *sink, hipStream_t s);
 hipError_t launch_sgemm(uint32_t M, uint32_t N, uint32_t K, const float *A, const float *B, float *C,

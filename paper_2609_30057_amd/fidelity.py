@@ -1,0 +1,152 @@
+"""Shared-GPU timing fidelity: p95 inflation of probe kernels timed inside
+critical regions while sibling processes generate and check on the same GPU.
+
+Paper: Section 6.3 (Eq. 1, P = p95(t_measured / t_native) - 1, with a second
+native run as the control for run-to-run noise); Section 6.4 (fidelity by
+kernel duration, 0.1 / 1 / 10 ms); Section 6.5 (ungated sharing as the
+unprotected baseline); Section 6.6 (single-shot and median-of-ten timing).
+
+Procedure, on one GPU:
+  1. calibrate the probe's iteration count to each target duration, alone;
+  2. native: `samples` single-shot timings per duration, alone (each sample:
+     region entry, 1 warm-up, a 512 MiB flush, one timed launch, exit; then
+     a 5 ms off-region gap);
+  3. control: the same again (native repeat);
+  4. gated: the same while `siblings` processes loop generate -> inject ->
+     check on 512 MiB fp16 tensors (the check_stress command) off-region,
+     every submission through counter-and-gate;
+  5. ungated: the same with every process registered without gating, so
+     nothing excludes the siblings from the timed interval.
+t_native is the median of the native run per duration.
+"""
+import multiprocessing as mp
+import time
+import uuid
+
+import numpy as np
+
+from . import stats
+from . import workloads as W
+
+MIB = 1 << 20
+
+
+def _sibling(shm, gated, n, stop, ready, q):
+    import torch
+
+    import paper_2609_30057_amd as krex
+    torch.cuda.set_device(0)
+    krex.attach(0, shm_name=shm, gated=gated)
+    cfg = W.CHECK_STRESS
+    x = torch.empty(n, dtype=torch.float16, device="cuda:0")
+    y = torch.empty_like(x)
+    out = krex.check_result_buffer()
+    krex.gen(x, cfg["seed"], 0, "uniform", cfg["p0"], cfg["p1"])
+    torch.cuda.synchronize()
+    ready.set()
+    rounds = 0
+    t0 = time.perf_counter()
+    while not stop.is_set():
+        krex.gen(x, cfg["seed"], 0, "uniform", cfg["p0"], cfg["p1"])
+        krex.inject(y, x, cfg["mask_seed"], cfg["rate"], cfg["delta"], "exact")
+        krex.check(y, x, cfg["rtol"], cfg["atol"], out=out)       # reads the verdict: one round in flight
+        rounds += 1
+    dt = time.perf_counter() - t0
+    q.put((rounds, dt, krex.gate_stats()))
+    krex.detach()
+
+
+def _calibrate(krex, sink, target_ms):
+    iters = 20000
+    for _ in range(4):
+        t = float(np.median(krex.time_loop(krex.probe_launcher(iters, sink), 2, 7)))
+        iters = max(1, int(round(iters * target_ms / t)))
+    t = float(np.median(krex.time_loop(krex.probe_launcher(iters, sink), 2, 7)))
+    return iters, t
+
+
+def _measure(krex, plan, samples, fl, sink, gap_ms):
+    times, drains = {}, []
+    for d, iters in plan:
+        fn = krex.probe_launcher(iters, sink)
+        ts = []
+        for _ in range(samples):
+            ts.append(krex.time_loop(fn, 1, 1, flush_buf=fl, region=True)[0])
+            drains.append(krex.gate_stats()["last_drain_ns"] / 1e6)
+            time.sleep(gap_ms / 1e3)
+        times[d] = ts
+    return times, drains
+
+
+def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None):
+    import torch
+
+    import paper_2609_30057_amd as krex
+    cfg = W.SHARED
+    samples = samples or cfg["samples"]
+    durations_ms = durations_ms or cfg["probe_ms"]
+    siblings = cfg["siblings"] if siblings is None else siblings
+    n = sibling_elems or W.CHECK_STRESS["rows"] * W.CHECK_STRESS["cols"]
+    torch.cuda.set_device(0)
+    fl = torch.empty(cfg["flush_bytes"] // 4, dtype=torch.int32, device="cuda:0")
+    sink = torch.empty(krex.PROBE_THREADS, dtype=torch.float32, device="cuda:0")
+    ctx = mp.get_context("spawn")
+    result = {"metric": "p95 in-region timing inflation (Eq. 1)", "unit": "%", "samples": samples,
+              "siblings": siblings, "sibling_workload": "check_stress gen+inject+check, %d fp16 elements" % n,
+              "flush_bytes": cfg["flush_bytes"], "gap_ms": cfg["gap_ms"], "P": {}, "P_median_of_10": {},
+              "median_ratio": {}, "within_5pct": {}, "calibrated": {}, "sibling_GBps": {}, "drain_ms": {}}
+    times = {}
+    for mode in ("native", "control", "gated", "ungated"):
+        gated = mode != "ungated"
+        shm = "/krex-fid-%s" % uuid.uuid4().hex[:10]
+        krex.attach(0, shm_name=shm, gated=gated)
+        if mode == "native":
+            plan = []
+            for d in durations_ms:
+                iters, t = _calibrate(krex, sink, d)
+                plan.append((d, iters))
+                result["calibrated"][str(d)] = {"iters": iters, "ms": round(t, 4)}
+        procs, stop, q = [], ctx.Event(), ctx.Queue()
+        if mode in ("gated", "ungated"):
+            readies = []
+            for _ in range(siblings):
+                ready = ctx.Event()
+                p = ctx.Process(target=_sibling, args=(shm, gated, n, stop, ready, q))
+                p.start()
+                procs.append(p)
+                readies.append(ready)
+            for r in readies:
+                if not r.wait(600):
+                    raise RuntimeError("sibling did not start")
+        t0 = time.perf_counter()
+        times[mode], drains = _measure(krex, plan, samples, fl, sink, cfg["gap_ms"])
+        wall = time.perf_counter() - t0
+        if procs:
+            stop.set()
+            got = [q.get(timeout=300) for _ in procs]
+            for p in procs:
+                p.join(120)
+            rounds = sum(g[0] for g in got)
+            secs = max(g[1] for g in got)
+            result["sibling_GBps"][mode] = round(rounds * 10 * n / secs / 1e9, 1)
+            result["sibling_parks"] = result.get("sibling_parks", {})
+            result["sibling_parks"][mode] = int(sum(g[2]["parks"] for g in got))
+        d = np.asarray(drains)
+        result["drain_ms"][mode] = {"p50": round(float(np.median(d)), 4), "p95": round(float(np.percentile(d, 95)), 4),
+                                    "max": round(float(d.max()), 4)}
+        result.setdefault("wall_s", {})[mode] = round(wall, 1)
+        krex.detach()
+    for d in durations_ms:
+        native = float(np.median(times["native"][d]))
+        key = str(d)
+        result["P"][key] = {m: round(100 * stats.p95_inflation(times[m][d], native), 3)
+                            for m in ("control", "gated", "ungated")}
+        nat10 = float(np.median(stats.medians_of(times["native"][d])))
+        result["P_median_of_10"][key] = {m: round(100 * stats.p95_inflation(stats.medians_of(times[m][d]), nat10), 3)
+                                         for m in ("control", "gated", "ungated")}
+        result["median_ratio"][key] = {m: round(stats.median_ratio(times[m][d], native), 4)
+                                       for m in ("control", "gated", "ungated")}
+        result["within_5pct"][key] = {m: round(stats.within(times[m][d], native), 4)
+                                      for m in ("control", "gated", "ungated")}
+        result["calibrated"][key]["native_median_ms"] = round(native, 4)
+    return result

@@ -106,3 +106,15 @@ def test_rejects_bad_tolerances(oracle_mod):
     for rt, at in ((-1.0, 0.0), (0.0, float("nan")), (float("inf"), 0.0)):
         with pytest.raises(ValueError):
             oracle_mod.check(x, "f32", x, "f32", rt, at)
+
+
+def test_overflowed_difference_matches_torch():
+    """torch.isclose never calls an infinite difference close, even when the
+    tolerance overflows too."""
+    a = np.array([-3.0e38, 3.0e38, 1.0], dtype=np.float32)
+    b = np.array([3.0e38, -3.0e38, 1.5], dtype=np.float32)
+    for rtol in (2.0, 10.0):
+        close = torch.isclose(torch.from_numpy(a), torch.from_numpy(b), rtol=rtol, atol=0.0)
+        import oracle
+        r = oracle.check(a, "f32", b, "f32", rtol, 0.0)
+        assert r["mismatches"] == int((~close).sum()) == 2

@@ -80,10 +80,12 @@ def test_upcast_every_pattern(oracle_mod, name, nbits):
 
 def test_fp8_named_points(oracle_mod):
     """e4m3fn facts: max 448, min subnormal 2^-9, 464 is the tie that rounds
-    down to 448, anything rounding past it is NaN, infinity is NaN."""
+    down to 448, anything rounding past it is NaN, infinity is NaN; a NaN
+    input gives the canonical NaN 0x7F whatever its sign."""
     cases = [(448.0, 0x7E), (464.0, 0x7E), (465.0, 0x7F), (480.0, 0x7F), (float("inf"), 0x7F),
              (-448.0, 0xFE), (-1000.0, 0xFF), (2.0**-9, 0x01), (2.0**-10, 0x00), (1.5 * 2.0**-10, 0x01),
-             (2.0**-6, 0x08), (1.0, 0x38), (0.0, 0x00), (-0.0, 0x80)]
+             (2.0**-6, 0x08), (1.0, 0x38), (0.0, 0x00), (-0.0, 0x80), (float("nan"), 0x7F),
+             (-float("nan"), 0x7F)]
     x = np.array([c[0] for c in cases], dtype=np.float32)
     got = oracle_mod.from_f32(x, "f8")
     assert [int(v) for v in got] == [c[1] for c in cases]
