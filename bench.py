@@ -19,11 +19,11 @@ measured by `--fidelity` (Section 6.3, Eq. 1), which prints its own line.
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
        python bench.py --fidelity [--samples S]
        python bench.py --kernels          per-kernel throughput on the command shapes
+       python bench.py --configs          the other commands: gemm_tiny, check_stress, mixed_stream
        python bench.py --calib-copy       also time a plain 1 GiB device copy (the
                                           reference kernel for rocprofv3 byte counters)
 """
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -39,11 +39,6 @@ GIB = 1 << 30
 PROFILES = os.path.join(ROOT, "profiles")
 
 
-def _sha256(path):
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
-
-
 def _traffic_for(kernel_key):
     """HBM bytes per launch from the committed rocprofv3 PMC summary, or None
     when it is missing or the kernel source changed since it was taken."""
@@ -53,8 +48,8 @@ def _traffic_for(kernel_key):
     with open(path) as f:
         data = json.load(f)
     ent = data.get(kernel_key)
-    src = os.path.join(ROOT, "paper_2609_30057_amd", "csrc", "kernels.hip")
-    if not ent or ent.get("kernels_hip_sha256") != _sha256(src):
+    from paper_2609_30057_amd.profiling import kernel_source_sha
+    if not ent or ent.get("source_sha256") != kernel_source_sha(kernel_key.split("/")[0]):
         return None
     return ent.get("hbm_bytes_per_launch")
 
@@ -275,6 +270,113 @@ def run_kernels():
             "peak_GBps": HBM_PEAK_GBPS, "kernels": res}
 
 
+def run_configs():
+    """The other commands end to end: gemm_tiny (gen + check + 100 reps with a
+    512 MiB flush in a region), check_stress (gen + inject + check of 256M
+    fp16), mixed_stream (64 derived commands: gen, inject, check with the
+    verdict read back, 512 MiB flush). GB/s = algorithmic bytes / summed
+    event time of the hot-path kernels; mixed_stream also reports wall
+    commands/s including launches and verdict readback."""
+    import numpy as np
+    import torch
+
+    import paper_2609_30057_amd as krex
+    from paper_2609_30057_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    shm = "/krex-cfg-%s" % uuid.uuid4().hex[:10]
+    krex.attach(0, shm_name=shm)
+    out = {"metric": "per-command gen+check+flush GB/s", "unit": "GB/s", "commands": {}}
+    res = krex.check_result_buffer(dev)
+
+    def ev():
+        e = torch.cuda.Event(enable_timing=True)
+        e.record()
+        return e
+
+    # gemm_tiny
+    cfg = W.GEMM_TINY
+    n = cfg["n"]
+    offA, offB = W.gemm_tiny_offsets()
+    A = torch.empty(n, n, device=dev)
+    B = torch.empty_like(A)
+    C = torch.empty_like(A)
+    fl512 = torch.empty(cfg["flush_bytes"] // 4, dtype=torch.int32, device=dev)
+    krex.gen(A, cfg["seed"], offA)
+    krex.gen(B, cfg["seed"], offB)
+    Cref = torch.matmul(A.cpu(), B.cpu()).to(dev)          # the command's fp32 CPU reference
+    krex.fixture_sgemm(A, B, C)
+    e0 = ev()
+    krex.gen(A, cfg["seed"], offA)
+    krex.gen(B, cfg["seed"], offB)
+    e1 = ev()
+    krex.check(C.view(-1), Cref.view(-1), cfg["rtol"], cfg["atol"], out=res, sync=False)
+    e2 = ev()
+    times, ftimes = krex.time_loop(krex.sgemm_launcher(A, B, C), cfg["warmup"], cfg["reps"], flush_buf=fl512,
+                                   region=True, with_flush_times=True)
+    v = krex.decode_check_result(res)
+    t = (e0.elapsed_time(e1) + e1.elapsed_time(e2) + sum(ftimes)) / 1e3
+    nbytes = 2 * n * n * 4 + n * n * 8 + cfg["reps"] * cfg["flush_bytes"]
+    out["commands"]["gemm_tiny"] = {"GBps": round(nbytes / t / 1e9, 1), "bytes": nbytes,
+                                    "candidate_median_ms": round(float(np.median(times)), 4),
+                                    "mismatches": v.mismatches, "max_abs": v.max_abs}
+    del A, B, C, Cref
+
+    # check_stress
+    cfg = W.CHECK_STRESS
+    m = cfg["rows"] * cfg["cols"]
+    x = torch.empty(m, dtype=torch.float16, device=dev)
+    y = torch.empty_like(x)
+    for _ in range(2):
+        e0 = ev()
+        krex.gen(x, cfg["seed"], 0, "uniform", cfg["p0"], cfg["p1"])
+        e1 = ev()
+        krex.inject(y, x, cfg["mask_seed"], cfg["rate"], cfg["delta"], "exact")
+        e2 = ev()
+        krex.check(y, x, cfg["rtol"], cfg["atol"], out=res, sync=False)
+        e3 = ev()
+        v = krex.decode_check_result(res)
+    tg, ti, tc = e0.elapsed_time(e1), e1.elapsed_time(e2), e2.elapsed_time(e3)
+    nbytes = m * 2 + m * 4 + m * 4
+    out["commands"]["check_stress"] = {
+        "GBps": round(nbytes / ((tg + ti + tc) / 1e3) / 1e9, 1), "bytes": nbytes,
+        "gen_GBps": round(m * 2 / (tg / 1e3) / 1e9, 1), "inject_GBps": round(m * 4 / (ti / 1e3) / 1e9, 1),
+        "check_GBps": round(m * 4 / (tc / 1e3) / 1e9, 1), "mismatches": v.mismatches, "max_abs": v.max_abs,
+        "argmax_abs": v.argmax_abs}
+
+    # mixed_stream
+    cfg = W.MIXED_STREAM
+    w = torch.empty(1024, dtype=torch.int32, device=dev)
+    krex.gen(w, cfg["seed"], 0)
+    cmds = W.mixed_stream_commands(w.cpu().numpy().view(np.uint32))
+    del x, y
+    xbuf = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    ybuf = torch.empty_like(xbuf)
+    tdt = {0: torch.float32, 1: torch.bfloat16, 2: torch.float16, 3: torch.float8_e4m3fn}
+    torch.cuda.synchronize()
+    kernel_ms, total = 0.0, 0
+    t0 = time.perf_counter()
+    for c in cmds:
+        xv = xbuf[:c.nbytes].view(tdt[c.dtype])
+        yv = ybuf[:c.nbytes].view(tdt[c.dtype])
+        e0 = ev()
+        krex.gen(xv, c.value_seed, 0, c.dist, c.p0, c.p1)
+        krex.inject(yv, xv, c.mask_seed, c.rate, cfg["delta"], "round")
+        krex.check(yv, xv, c.rtol, c.atol, out=res, sync=False)
+        krex.flush(fl512)
+        e1 = ev()
+        krex.decode_check_result(res)
+        kernel_ms += e0.elapsed_time(e1)
+        total += c.nbytes * 5 + cfg["flush_bytes"]
+    wall = time.perf_counter() - t0
+    out["commands"]["mixed_stream"] = {"GBps": round(total / (kernel_ms / 1e3) / 1e9, 1), "bytes": total,
+                                       "wall_GBps": round(total / wall / 1e9, 1),
+                                       "commands_per_s": round(len(cmds) / wall, 1)}
+    krex.detach()
+    return out
+
+
 def run_copy_calibration():
     """A plain device-to-device copy of 1 GiB, three times: the kernel whose
     rocprofv3 FETCH_SIZE / WRITE_SIZE readings calibrate the byte counters."""
@@ -296,6 +398,7 @@ def main():
     ap.add_argument("--samples", type=int, default=None)
     ap.add_argument("--kernels", action="store_true")
     ap.add_argument("--calib-copy", action="store_true")
+    ap.add_argument("--configs", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (use --gpus 1)", file=sys.stderr)
@@ -306,6 +409,9 @@ def main():
         return
     if args.kernels:
         print(json.dumps(run_kernels()), flush=True)
+        return
+    if args.configs:
+        print(json.dumps(run_configs()), flush=True)
         return
     out = run_gemm_large(args.steps, args.warmup, not args.no_cpu_baseline)
     if args.calib_copy:

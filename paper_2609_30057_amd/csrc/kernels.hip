@@ -712,8 +712,9 @@ static hipError_t check_ab(const void *a, const void *b, uint64_t n, float rtol,
     const bool vec = (((uintptr_t)a & 15u) == 0 && ((uintptr_t)b & 15u) == 0);
     const uint64_t nchunks = n / E;
     // Chunks per thread: enough that the grid stays within the partial
-    // buffer, at least the tuning floor.
-    static const uint32_t u_floor = tune_env("KREX_CHECK_U", 1);
+    // buffer, and at least 8 so that the per-lane re-read of the best chunk
+    // adds at most 1/8 to the bytes read (and the pipeline has depth).
+    static const uint32_t u_floor = tune_env("KREX_CHECK_U", 8);
     uint64_t U = (nchunks + (uint64_t)kThreads * kMaxCheckBlocks - 1) / ((uint64_t)kThreads * kMaxCheckBlocks);
     if (U < u_floor) U = u_floor;
     if (U == 0) U = 1;

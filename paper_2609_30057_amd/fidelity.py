@@ -20,6 +20,7 @@ Procedure, on one GPU:
 t_native is the median of the native run per duration.
 """
 import multiprocessing as mp
+import sys
 import time
 import uuid
 
@@ -136,6 +137,7 @@ def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None):
                                     "max": round(float(d.max()), 4)}
         result.setdefault("wall_s", {})[mode] = round(wall, 1)
         krex.detach()
+        print("fidelity: %s done (%.1f s)" % (mode, wall), file=sys.stderr, flush=True)
     for d in durations_ms:
         native = float(np.median(times["native"][d]))
         key = str(d)

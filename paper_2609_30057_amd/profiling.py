@@ -14,11 +14,30 @@ import glob
 import hashlib
 import json
 import os
+import re
 import statistics
 
 GIB = 1 << 30
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 KERNELS_HIP = os.path.join(ROOT, "paper_2609_30057_amd", "csrc", "kernels.hip")
+DEVICE_HPP = os.path.join(ROOT, "paper_2609_30057_amd", "csrc", "krex_device.hpp")
+
+# kernels.hip is split into sections by "// ---- <name>" rules; a traffic
+# figure is tied to the source of its kernel's section (plus the device
+# header for the kernels that use its conversions and transforms).
+SECTION_OF = {"k_flush": "flush", "k_check": "check", "k_check_final": "check", "k_gen": "generation",
+              "k_inject": "injection", "k_xform": "words transform", "k_probe": "probe", "k_sgemm": "fixture"}
+
+
+def kernel_source_sha(kernel):
+    """sha256 of the source that defines `kernel` (short name, e.g. k_flush)."""
+    text = open(KERNELS_HIP).read()
+    parts = re.split(r"^// -{10,} (.+?)\s*$", text, flags=re.M)
+    sections = {parts[i].strip(): parts[i + 1] for i in range(1, len(parts) - 1, 2)}
+    body = sections[SECTION_OF[kernel]]
+    if kernel not in ("k_flush", "k_probe", "k_sgemm"):
+        body += open(DEVICE_HPP).read()
+    return hashlib.sha256(body.encode()).hexdigest()
 
 
 def _rows(path):
@@ -75,7 +94,6 @@ def cmd_traffic(a):
     w_copy = statistics.median(write[ck]) * 1024.0
     sf, sw = GIB / f_copy, GIB / w_copy
     algo = json.loads(a.algo) if a.algo else {}
-    sha = hashlib.sha256(open(KERNELS_HIP, "rb").read()).hexdigest()
     data = {"calibration": {"kernel": _short(ck), "fetch_bytes": f_copy, "write_bytes": w_copy,
                             "fetch_scale": sf, "write_scale": sw}}
     lines = ["# HBM traffic per dispatch (rocprofv3 FETCH_SIZE / WRITE_SIZE): %s" % a.title, "",
@@ -95,9 +113,10 @@ def cmd_traffic(a):
         lines.append("| `%s` | %d | %.1f | %.1f | %s | %s |" % (
             key, len(fetch[k]), fb / 2**20, wb / 2**20, "%.1f" % (al / 2**20) if al else "-",
             "%.3f" % ((fb + wb) / al) if al else "-"))
-        data["%s/%s" % (key.split("::")[-1].split("<")[0], a.workload)] = {
+        short = key.split("::")[-1].split("<")[0]
+        data["%s/%s" % (short, a.workload)] = {
             "kernel": key, "hbm_bytes_per_launch": round(fb + wb), "fetch_bytes": round(fb), "write_bytes": round(wb),
-            "algorithmic_bytes": al, "kernels_hip_sha256": sha}
+            "algorithmic_bytes": al, "source_sha256": kernel_source_sha(short) if short in SECTION_OF else None}
     with open(a.out, "w") as f:
         f.write("\n".join(lines) + "\n")
     with open(a.out_json, "w") as f:
