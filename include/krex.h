@@ -96,9 +96,19 @@ typedef struct krex_check_result {
  * "/krex-" + the device's PCI bus id). The first process creates and
  * initialises it. flags: KREX_ATTACH_NO_GATE registers without gating (the
  * ungated control configuration of Section 6.1); the process can still
- * enter regions. Returns KREX_ESTATE if already attached, KREX_EPEER if the
- * segment has another layout version, KREX_ESYS on a POSIX failure. */
+ * enter regions. KREX_ATTACH_CPU_EXCLUSIVE adds CPU exclusivity to this
+ * process's regions (Section 4.2, steps 4, 5 and 7): after the drain it
+ * stops the process tree of every other registered process with SIGSTOP and
+ * pins the entering thread to one core of its affinity set (the core named
+ * by the KREX_REGION_CPU environment variable if it is in the set, else the
+ * highest-numbered one); region exit resumes them with SIGCONT and restores
+ * the affinity before the gate reopens. A holder that dies inside such a
+ * region has its stopped siblings resumed by the process that recovers the
+ * lock. Returns KREX_EINVAL for unknown flags, KREX_ESTATE if already
+ * attached, KREX_EPEER if the segment has another layout version,
+ * KREX_ESYS on a POSIX failure. */
 #define KREX_ATTACH_NO_GATE 1u
+#define KREX_ATTACH_CPU_EXCLUSIVE 2u
 krex_status krex_attach(int32_t device, const char *shm_name, uint32_t flags);
 
 /* Waits for this process's in-flight work, releases its slot and the
@@ -232,6 +242,7 @@ typedef struct krex_gate_stats {
     uint64_t parks;            /* submissions of this process that waited at a closed gate */
     uint64_t park_ns;          /* time spent waiting there */
     uint64_t recoveries;       /* dead holders recovered by this process */
+    uint64_t last_frozen;      /* processes stopped at the last entry (CPU exclusivity) */
     int32_t slot;              /* this process's registration slot, -1 if none */
     int32_t gated;             /* 1 if submissions are gated */
 } krex_gate_stats;

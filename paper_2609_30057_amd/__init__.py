@@ -28,6 +28,7 @@ UNIFORM, NORMAL, BITCAST = 0, 1, 2
 INJ_ROUND, INJ_EXACT = 0, 1
 TL_REGION = 1
 ATTACH_NO_GATE = 1
+ATTACH_CPU_EXCLUSIVE = 2
 PROBE_THREADS = 65536
 
 OK, RECOVERED = 0, 1
@@ -66,7 +67,8 @@ class _SgemmArgs(ctypes.Structure):
 class _GateStats(ctypes.Structure):
     _fields_ = [("regions", ctypes.c_uint64), ("last_drain_ns", ctypes.c_uint64),
                 ("total_drain_ns", ctypes.c_uint64), ("parks", ctypes.c_uint64), ("park_ns", ctypes.c_uint64),
-                ("recoveries", ctypes.c_uint64), ("slot", ctypes.c_int32), ("gated", ctypes.c_int32)]
+                ("recoveries", ctypes.c_uint64), ("last_frozen", ctypes.c_uint64),
+                ("slot", ctypes.c_int32), ("gated", ctypes.c_int32)]
 
 
 LAUNCH_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_void_p)
@@ -260,12 +262,15 @@ def fixture_sgemm(A, B, C, stream=None):
 
 # ----------------------------------------------------------------------- regions
 
-def attach(device=None, shm_name=None, gated=True):
-    """Registers this process with its GPU's region coordinator (Section 4.2)."""
+def attach(device=None, shm_name=None, gated=True, cpu_exclusive=False):
+    """Registers this process with its GPU's region coordinator (Section 4.2).
+    ``cpu_exclusive`` makes this process's regions stop the other registered
+    process trees and pin the entering thread (Section 4.2, steps 4-5, 7)."""
     if device is None:
         device = _torch().cuda.current_device()
     name = shm_name.encode() if shm_name else None
-    return _chk(lib().krex_attach(device, name, 0 if gated else ATTACH_NO_GATE), "krex_attach")
+    flags = (0 if gated else ATTACH_NO_GATE) | (ATTACH_CPU_EXCLUSIVE if cpu_exclusive else 0)
+    return _chk(lib().krex_attach(device, name, flags), "krex_attach")
 
 
 def detach():

@@ -277,7 +277,7 @@ extern "C" {
 
 krex_status krex_attach(int32_t device, const char *shm_name, uint32_t flags)
 {
-    if (flags & ~KREX_ATTACH_NO_GATE) return KREX_EINVAL;
+    if (flags & ~(KREX_ATTACH_NO_GATE | KREX_ATTACH_CPU_EXCLUSIVE)) return KREX_EINVAL;
     char name[256];
     if (shm_name) {
         if (strlen(shm_name) >= sizeof name) return KREX_EINVAL;
@@ -290,7 +290,9 @@ krex_status krex_attach(int32_t device, const char *shm_name, uint32_t flags)
             if (*p == ':' || *p == '.') *p = '_';
         snprintf(name, sizeof name, "/krex-%s", bus);
     }
-    const int rc = krexg::attach(name, (flags & KREX_ATTACH_NO_GATE) ? krexg::kNoGate : 0u);
+    const uint32_t gf = ((flags & KREX_ATTACH_NO_GATE) ? krexg::kNoGate : 0u) |
+                        ((flags & KREX_ATTACH_CPU_EXCLUSIVE) ? krexg::kCpuExclusive : 0u);
+    const int rc = krexg::attach(name, gf);
     if (rc == KREX_OK) g_device_attached = device;
     return rc;
 }
@@ -522,6 +524,7 @@ krex_status krex_get_gate_stats(krex_gate_stats *out)
     out->parks = st.parks;
     out->park_ns = st.park_ns;
     out->recoveries = st.recoveries;
+    out->last_frozen = st.last_frozen;
     out->slot = st.slot;
     out->gated = st.gated;
     return KREX_OK;

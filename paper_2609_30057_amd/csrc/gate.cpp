@@ -6,6 +6,7 @@
 #include <fcntl.h>
 #include <linux/futex.h>
 #include <pthread.h>
+#include <sched.h>
 #include <signal.h>
 #include <stdio.h>
 #include <stdlib.h>
@@ -15,6 +16,8 @@
 #include <sys/syscall.h>
 #include <time.h>
 #include <unistd.h>
+
+#include <dirent.h>
 
 #include <atomic>
 #include <climits>
@@ -26,7 +29,7 @@ namespace krexg {
 namespace {
 
 constexpr uint64_t kMagic = 0x4b52455847415445ull;   // "KREXGATE"
-constexpr uint32_t kVersion = 3;
+constexpr uint32_t kVersion = 4;
 constexpr uint64_t kEpochMask = (1ull << 48) - 1;
 
 struct alignas(64) Slot {
@@ -34,6 +37,7 @@ struct alignas(64) Slot {
     std::atomic<uint32_t> flags;       // kNoGate
     std::atomic<uint64_t> start_time;  // /proc start time of pid, guards pid reuse
     std::atomic<int64_t> inflight;     // counted submissions not yet completed
+    std::atomic<uint64_t> frozen_by;   // gate word of the region that stopped this process; 0 = running
 };
 
 struct Segment {
@@ -57,8 +61,13 @@ struct State {
     int slot = -1;
     bool gated_ = false;
     bool in_region = false;
+    uint32_t flags = 0;
     uint32_t spin_us = 50;
+    uint64_t region_gate = 0;          // gate word of this process's current region
+    bool pinned = false;
+    cpu_set_t saved_affinity;
     std::atomic<uint64_t> regions{0}, last_drain_ns{0}, total_drain_ns{0}, parks{0}, park_ns{0}, recoveries{0};
+    std::atomic<uint64_t> last_frozen{0};
 };
 
 State &st()
@@ -127,6 +136,111 @@ bool alive(int32_t pid, uint64_t start)
 
 inline uint32_t holder_of(uint64_t g) { return (uint32_t)(g >> 48); }
 
+// Scheduler state letter of a process (field 3 of /proc/<pid>/stat), 0 if
+// the process is gone.
+char proc_state(int32_t pid)
+{
+    char path[64];
+    snprintf(path, sizeof path, "/proc/%d/stat", (int)pid);
+    FILE *f = fopen(path, "r");
+    if (!f) return 0;
+    char buf[512];
+    size_t n = fread(buf, 1, sizeof buf - 1, f);
+    fclose(f);
+    buf[n] = 0;
+    const char *p = strrchr(buf, ')');
+    return (p && p[1] == ' ') ? p[2] : 0;
+}
+
+// Waits (bounded) until a signalled process has actually stopped, so that it
+// cannot fork between the signal and the enumeration of its children.
+void wait_stopped(int32_t pid, uint64_t until)
+{
+    while (now_ns() < until) {
+        const char c = proc_state(pid);
+        if (c == 'T' || c == 't' || c == 0 || c == 'Z' || c == 'X') return;
+        cpu_relax();
+    }
+}
+
+// Direct children of every thread of `pid` (/proc/<pid>/task/<tid>/children).
+int children_of(int32_t pid, int32_t *out, int max)
+{
+    char path[64];
+    snprintf(path, sizeof path, "/proc/%d/task", (int)pid);
+    DIR *d = opendir(path);
+    if (!d) return 0;
+    int n = 0;
+    while (dirent *e = readdir(d)) {
+        if (e->d_name[0] < '0' || e->d_name[0] > '9') continue;
+        char cp[96];
+        snprintf(cp, sizeof cp, "/proc/%d/task/%s/children", (int)pid, e->d_name);
+        FILE *f = fopen(cp, "r");
+        if (!f) continue;
+        int c;
+        while (n < max && fscanf(f, "%d", &c) == 1) out[n++] = c;
+        fclose(f);
+    }
+    closedir(d);
+    return n;
+}
+
+constexpr int kMaxTree = 256;
+
+// Stops the process tree rooted at `root` top-down, each parent stopped
+// before its children are listed, never stopping `self` or anything below it
+// (a holder may itself descend from a registered sibling). Returns the number
+// of processes signalled.
+int freeze_tree(int32_t root, int32_t self, uint64_t until)
+{
+    int32_t q[kMaxTree];
+    int head = 0, tail = 0, count = 0;
+    if (root == self) return 0;
+    q[tail++] = root;
+    while (head < tail) {
+        const int32_t p = q[head++];
+        if (kill(p, SIGSTOP) != 0) continue;
+        ++count;
+        wait_stopped(p, until);
+        int32_t kids[kMaxTree];
+        const int k = children_of(p, kids, kMaxTree);
+        for (int i = 0; i < k && tail < kMaxTree; ++i)
+            if (kids[i] != self) q[tail++] = kids[i];
+    }
+    return count;
+}
+
+// Resumes the tree rooted at `root`: descendants first (listed while the
+// tree is still stopped), the root last.
+void thaw_tree(int32_t root, int32_t self)
+{
+    int32_t q[kMaxTree];
+    int head = 0, tail = 0;
+    q[tail++] = root;
+    while (head < tail) {
+        int32_t kids[kMaxTree];
+        const int k = children_of(q[head++], kids, kMaxTree);
+        for (int i = 0; i < k && tail < kMaxTree; ++i)
+            if (kids[i] != self) q[tail++] = kids[i];
+    }
+    for (int i = tail - 1; i >= 0; --i) kill(q[i], SIGCONT);
+}
+
+// Resumes every registered process tree stopped by the region whose gate
+// word is `g` (Section 4.2, step 7 and holder-death cleanup: bound to the
+// holder and epoch, so a late cleanup never undoes a later region's freeze).
+void thaw_region(Segment *seg, uint64_t g)
+{
+    const int32_t self = (int32_t)getpid();
+    for (int i = 0; i < kSlots; ++i) {
+        Slot &sl = seg->slots[i];
+        if (sl.frozen_by.load() != g) continue;
+        const int32_t pid = sl.pid.load();
+        if (pid > 0 && alive(pid, sl.start_time.load())) thaw_tree(pid, self);
+        sl.frozen_by.store(0);
+    }
+}
+
 void open_gate(Segment *seg, uint64_t epoch)
 {
     seg->gate.store(epoch & kEpochMask, std::memory_order_seq_cst);
@@ -142,6 +256,7 @@ void recover_dead_holder(Segment *seg)
     const uint64_t g = seg->gate.load(std::memory_order_seq_cst);
     const uint32_t h = holder_of(g);
     if (h != 0) {
+        thaw_region(seg, g);
         Slot &s = seg->slots[h - 1];
         const int32_t pid = s.pid.load();
         if (pid == 0 || !alive(pid, s.start_time.load())) {
@@ -253,7 +368,11 @@ void at_exit_release()
     State &s = st();
     if (!s.seg || s.slot < 0) return;
     Segment *seg = s.seg;
+    // A forked child inherits this state but not the registration: only the
+    // registered process releases its slot and region.
+    if (seg->slots[s.slot].pid.load() != (int32_t)getpid()) return;
     if (s.in_region) {
+        thaw_region(seg, s.region_gate);
         open_gate(seg, seg->epoch.load());
         pthread_mutex_unlock(&seg->lock);
         s.in_region = false;
@@ -298,11 +417,13 @@ int attach(const char *shm_name, uint32_t flags)
     }
     Slot &sl = seg->slots[slot];
     sl.start_time.store(start);
-    sl.flags.store(flags & kNoGate);
+    sl.flags.store(flags & (kNoGate | kCpuExclusive));
     sl.inflight.store(0);
+    sl.frozen_by.store(0);
     s.seg = seg;
     s.slot = slot;
     s.gated_ = (flags & kNoGate) == 0;
+    s.flags = flags;
     s.in_region = false;
     s.regions.store(0);
     s.last_drain_ns.store(0);
@@ -481,6 +602,42 @@ int region_begin(uint32_t timeout_ms)
     s.last_drain_ns.store(drain);
     s.total_drain_ns.fetch_add(drain);
     s.regions.fetch_add(1);
+    s.region_gate = seg->gate.load(std::memory_order_seq_cst);
+    s.last_frozen.store(0);
+    if (s.flags & kCpuExclusive) {
+        // Step 4: stop the siblings' process trees once their GPU work has
+        // drained, recording in each slot the region that stopped it so that
+        // cleanup after this holder's death resumes exactly these.
+        const int32_t self = (int32_t)getpid();
+        const uint64_t until = now_ns() + 20000000ull;
+        uint64_t frozen = 0;
+        for (int i = 0; i < kSlots; ++i) {
+            if (i == s.slot) continue;
+            Slot &sl = seg->slots[i];
+            const int32_t pid = sl.pid.load();
+            if (pid <= 0 || pid == self || !alive(pid, sl.start_time.load())) continue;
+            sl.frozen_by.store(s.region_gate);
+            frozen += (uint64_t)freeze_tree(pid, self, until);
+        }
+        s.last_frozen.store(frozen);
+        // Step 5 (second half): pin this thread to one core of its set.
+        if (sched_getaffinity(0, sizeof(cpu_set_t), &s.saved_affinity) == 0) {
+            int core = -1;
+            if (const char *e = getenv("KREX_REGION_CPU")) core = atoi(e);
+            if (core < 0 || !CPU_ISSET(core, &s.saved_affinity))
+                for (int c = CPU_SETSIZE - 1; c >= 0; --c)
+                    if (CPU_ISSET(c, &s.saved_affinity)) {
+                        core = c;
+                        break;
+                    }
+            if (core >= 0) {
+                cpu_set_t one;
+                CPU_ZERO(&one);
+                CPU_SET(core, &one);
+                s.pinned = sched_setaffinity(0, sizeof(cpu_set_t), &one) == 0;
+            }
+        }
+    }
     s.in_region = true;
     return status;
 }
@@ -492,7 +649,13 @@ int region_end()
     Segment *seg = s.seg;
     if (!seg) return KREX_ENOTATTACHED;
     if (!s.in_region) return KREX_ESTATE;
-    // Step 8: reopen the gate, wake parked siblings, release the lock.
+    // Step 7: resume stopped siblings and unpin; step 8: reopen the gate,
+    // wake parked siblings, release the lock.
+    if (s.flags & kCpuExclusive) thaw_region(seg, s.region_gate);
+    if (s.pinned) {
+        sched_setaffinity(0, sizeof(cpu_set_t), &s.saved_affinity);
+        s.pinned = false;
+    }
     open_gate(seg, seg->gate.load() & kEpochMask);
     s.in_region = false;
     pthread_mutex_unlock(&seg->lock);
@@ -508,6 +671,7 @@ void get_stats(Stats *out)
     out->parks = s.parks.load();
     out->park_ns = s.park_ns.load();
     out->recoveries = s.recoveries.load();
+    out->last_frozen = s.last_frozen.load();
     out->slot = s.slot;
     out->gated = s.seg && s.gated_ ? 1 : 0;
 }

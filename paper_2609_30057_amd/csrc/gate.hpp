@@ -13,7 +13,11 @@
 // and releases the lock before returning (Section 4.2, entry failure); a
 // holder that dies is recovered by the next process that takes the lock
 // (Section 4.2, holder death; here the robust mutex serialises recovery with
-// normal exit).
+// normal exit). With CPU exclusivity the holder also stops the siblings'
+// processes after the drain and pins its own thread (Section 4.2, steps 4
+// and 5), and resumes them before the gate reopens (step 7); the stop is
+// SIGSTOP / SIGCONT of the registered processes, recorded in shared memory
+// so that recovery from the holder's death resumes them.
 //
 // This file is plain POSIX C++ (no HIP): the GPU-side completion tracking
 // lives in the ABI layer, and the CPU tests drive the same code with a fake
@@ -31,11 +35,13 @@ struct Stats {
     uint64_t parks;
     uint64_t park_ns;
     uint64_t recoveries;
+    uint64_t last_frozen;
     int32_t slot;
     int32_t gated;
 };
 
 constexpr uint32_t kNoGate = 1u;          // register, never block or count
+constexpr uint32_t kCpuExclusive = 2u;    // as holder: stop siblings, pin the region thread
 constexpr int kSlots = 64;
 
 // All functions return krex status codes (KREX_OK, KREX_E*).

@@ -16,7 +16,10 @@ Procedure, on one GPU:
      check on 512 MiB fp16 tensors (the check_stress command) off-region,
      every submission through counter-and-gate;
   5. ungated: the same with every process registered without gating, so
-     nothing excludes the siblings from the timed interval.
+     nothing excludes the siblings from the timed interval;
+  6. frozen (optional): gated, and the holder's regions also stop the
+     siblings' process trees and pin the timing thread (CPU exclusivity,
+     Section 4.2 steps 4, 5 and 7).
 t_native is the median of the native run per duration.
 """
 import multiprocessing as mp
@@ -37,13 +40,13 @@ def _sibling(shm, gated, n, stop, ready, q):
 
     import paper_2609_30057_amd as krex
     torch.cuda.set_device(0)
-    krex.attach(0, shm_name=shm, gated=gated)
     cfg = W.CHECK_STRESS
     x = torch.empty(n, dtype=torch.float16, device="cuda:0")
     y = torch.empty_like(x)
     out = krex.check_result_buffer()
     krex.gen(x, cfg["seed"], 0, "uniform", cfg["p0"], cfg["p1"])
     torch.cuda.synchronize()
+    krex.attach(0, shm_name=shm, gated=gated)   # registered once initialised (Section 5)
     ready.set()
     rounds = 0
     t0 = time.perf_counter()
@@ -79,7 +82,7 @@ def _measure(krex, plan, samples, fl, sink, gap_ms):
     return times, drains
 
 
-def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None):
+def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, modes=None):
     import torch
 
     import paper_2609_30057_amd as krex
@@ -97,10 +100,12 @@ def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None):
               "flush_bytes": cfg["flush_bytes"], "gap_ms": cfg["gap_ms"], "P": {}, "P_median_of_10": {},
               "median_ratio": {}, "within_5pct": {}, "calibrated": {}, "sibling_GBps": {}, "drain_ms": {}}
     times = {}
-    for mode in ("native", "control", "gated", "ungated"):
+    modes = list(modes or ("native", "control", "gated", "ungated"))
+    compared = [m for m in modes if m != "native"]
+    for mode in ["native"] + compared:
         gated = mode != "ungated"
         shm = "/krex-fid-%s" % uuid.uuid4().hex[:10]
-        krex.attach(0, shm_name=shm, gated=gated)
+        krex.attach(0, shm_name=shm, gated=gated, cpu_exclusive=(mode == "frozen"))
         if mode == "native":
             plan = []
             for d in durations_ms:
@@ -108,7 +113,7 @@ def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None):
                 plan.append((d, iters))
                 result["calibrated"][str(d)] = {"iters": iters, "ms": round(t, 4)}
         procs, stop, q = [], ctx.Event(), ctx.Queue()
-        if mode in ("gated", "ungated"):
+        if mode in ("gated", "ungated", "frozen"):
             readies = []
             for _ in range(siblings):
                 ready = ctx.Event()
@@ -142,13 +147,13 @@ def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None):
         native = float(np.median(times["native"][d]))
         key = str(d)
         result["P"][key] = {m: round(100 * stats.p95_inflation(times[m][d], native), 3)
-                            for m in ("control", "gated", "ungated")}
+                            for m in compared}
         nat10 = float(np.median(stats.medians_of(times["native"][d])))
         result["P_median_of_10"][key] = {m: round(100 * stats.p95_inflation(stats.medians_of(times[m][d]), nat10), 3)
-                                         for m in ("control", "gated", "ungated")}
+                                         for m in compared}
         result["median_ratio"][key] = {m: round(stats.median_ratio(times[m][d], native), 4)
-                                       for m in ("control", "gated", "ungated")}
+                                       for m in compared}
         result["within_5pct"][key] = {m: round(stats.within(times[m][d], native), 4)
-                                      for m in ("control", "gated", "ungated")}
+                                      for m in compared}
         result["calibrated"][key]["native_median_ms"] = round(native, 4)
     return result

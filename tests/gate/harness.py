@@ -32,7 +32,8 @@ def build(variant=""):
 class Stats(ctypes.Structure):
     _fields_ = [("regions", ctypes.c_uint64), ("last_drain_ns", ctypes.c_uint64),
                 ("total_drain_ns", ctypes.c_uint64), ("parks", ctypes.c_uint64), ("park_ns", ctypes.c_uint64),
-                ("recoveries", ctypes.c_uint64), ("slot", ctypes.c_int32), ("gated", ctypes.c_int32)]
+                ("recoveries", ctypes.c_uint64), ("last_frozen", ctypes.c_uint64),
+                ("slot", ctypes.c_int32), ("gated", ctypes.c_int32)]
 
 
 def load(variant=""):

@@ -96,3 +96,69 @@ def submit_once(name, flags, timeout_ns, q):
     L.kg_wait_idle(10000)
     q.put(("submit", rc, t0, t.value, harness.stats(L)))
     L.kg_detach()
+
+
+def spinner(name, counter, child_counter, ready, stop):
+    """Registered process that spins on the CPU, with a forked child that
+    spins too (a process tree of two)."""
+    import os
+    L = _L()
+    assert L.kg_attach(name.encode(), 0) == OK
+    pid = os.fork()
+    if pid == 0:
+        while not stop.is_set():
+            child_counter.value += 1
+        os._exit(0)
+    ready.set()
+    while not stop.is_set():
+        counter.value += 1
+    os.waitpid(pid, 0)
+    L.kg_detach()
+
+
+def exclusive_holder(name, counters, regions, region_ms, q):
+    """Holder with CPU exclusivity: samples the siblings' counters inside and
+    after each region, and its own affinity inside and after."""
+    import os
+    L = _L()
+    assert L.kg_attach(name.encode(), 2) == OK
+    before = len(os.sched_getaffinity(0))
+    res = []
+    for _ in range(regions):
+        assert L.kg_region_begin(10000) == OK
+        aff_in = len(os.sched_getaffinity(0))
+        c0 = [c.value for c in counters]
+        time.sleep(region_ms / 1000)
+        c1 = [c.value for c in counters]
+        frozen = harness.stats(L)["last_frozen"]
+        assert L.kg_region_end() == OK
+        aff_out = len(os.sched_getaffinity(0))
+        time.sleep(0.05)
+        c2 = [c.value for c in counters]
+        res.append((c0, c1, c2, aff_in, aff_out, frozen))
+    q.put(("excl", before, res))
+    L.kg_detach()
+
+
+def exclusive_hold_and_die(name, ready):
+    L = _L()
+    assert L.kg_attach(name.encode(), 2) == OK
+    assert L.kg_region_begin(10000) == OK
+    ready.set()
+    time.sleep(600)
+
+
+def registered_parent_of_holder(name, counter, q):
+    """A registered process whose child is an exclusive holder: the holder
+    must not stop itself while stopping its parent's tree."""
+    import multiprocessing as mp
+    L = _L()
+    assert L.kg_attach(name.encode(), 0) == OK
+    ctx = mp.get_context("spawn")
+    cq = ctx.Queue()
+    child = ctx.Process(target=exclusive_holder, args=(name, [counter], 2, 100, cq))
+    child.start()
+    got = cq.get(timeout=60)
+    child.join(60)
+    q.put(("parent", child.exitcode, got))
+    L.kg_detach()

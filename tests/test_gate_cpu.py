@@ -227,3 +227,99 @@ def test_foreign_segment_rejected(shm_name):
         f.write(b"\0" * 100)
     L = harness.load()
     assert L.kg_attach(shm_name.encode(), 0) == EPEER
+
+
+def _stop_all(procs):
+    for p in procs:
+        if p.is_alive():
+            try:
+                os.kill(p.pid, signal.SIGCONT)
+            except ProcessLookupError:
+                pass
+
+
+def test_cpu_exclusive_region_stops_sibling_trees(shm_name):
+    """Section 4.2, steps 4, 5 and 7: inside a CPU-exclusive region the other
+    registered processes and their children make no CPU progress, the
+    entering thread runs on one core, and both are undone at exit."""
+    q = CTX.Queue()
+    stop = CTX.Event()
+    c_par = [CTX.RawValue("Q", 0) for _ in range(2)]
+    c_kid = [CTX.RawValue("Q", 0) for _ in range(2)]
+    readies = [CTX.Event() for _ in range(2)]
+    sibs = [CTX.Process(target=workers.spinner, args=(shm_name, c_par[i], c_kid[i], readies[i], stop))
+            for i in range(2)]
+    holder = None
+    try:
+        for p in sibs:
+            p.start()
+        for r in readies:
+            assert r.wait(60)
+        holder = CTX.Process(target=workers.exclusive_holder,
+                             args=(shm_name, c_par + c_kid, 4, 150, q))
+        holder.start()
+        tag, before, res = q.get(timeout=60)
+        holder.join(60)
+        assert holder.exitcode == 0
+    finally:
+        _stop_all(sibs + ([holder] if holder else []))
+        stop.set()
+    _join(sibs)
+    assert tag == "excl" and len(res) == 4
+    for c0, c1, c2, aff_in, aff_out, frozen in res:
+        assert c1 == c0, "a stopped process advanced inside the region: %s -> %s" % (c0, c1)
+        assert all(b > a for a, b in zip(c1, c2)), "not resumed after the region: %s -> %s" % (c1, c2)
+        assert aff_in == 1 and aff_out == before
+        assert frozen == 4                      # two registered processes, each with one child
+
+
+def test_dead_cpu_exclusive_holder_resumes_siblings(shm_name):
+    """Holder death (Section 4.2): the process that recovers the lock resumes
+    the process trees the dead holder had stopped."""
+    q = CTX.Queue()
+    stop = CTX.Event()
+    ready_s, ready_h = CTX.Event(), CTX.Event()
+    c, ck = CTX.RawValue("Q", 0), CTX.RawValue("Q", 0)
+    sib = CTX.Process(target=workers.spinner, args=(shm_name, c, ck, ready_s, stop))
+    holder = None
+    try:
+        sib.start()
+        assert ready_s.wait(60)
+        holder = CTX.Process(target=workers.exclusive_hold_and_die, args=(shm_name, ready_h))
+        holder.start()
+        assert ready_h.wait(60)
+        v0 = (c.value, ck.value)
+        time.sleep(0.2)
+        assert (c.value, ck.value) == v0            # stopped while the holder lives
+        os.kill(holder.pid, signal.SIGKILL)
+        holder.join(30)
+        b = CTX.Process(target=workers.try_region, args=(shm_name, 5000, q))
+        b.start()
+        tag, rc, _, st = q.get(timeout=60)
+        b.join(30)
+        assert tag == "try" and rc == RECOVERED and st["recoveries"] == 1
+        v1 = (c.value, ck.value)
+        time.sleep(0.2)
+        v2 = (c.value, ck.value)
+        assert v2[0] > v1[0] and v2[1] > v1[1]      # resumed by the recovery
+    finally:
+        _stop_all([sib] + ([holder] if holder else []))
+        stop.set()
+    _join([sib])
+
+
+def test_cpu_exclusive_holder_below_registered_parent(shm_name):
+    """A holder whose parent is registered stops that parent's tree but not
+    itself, so its regions complete."""
+    q = CTX.Queue()
+    dummy = CTX.RawValue("Q", 0)
+    parent = CTX.Process(target=workers.registered_parent_of_holder, args=(shm_name, dummy, q))
+    try:
+        parent.start()
+        tag, exitcode, got = q.get(timeout=120)
+    finally:
+        _stop_all([parent])
+    _join([parent])
+    assert tag == "parent" and exitcode == 0
+    assert got[0] == "excl" and len(got[2]) == 2
+    assert all(r[5] >= 1 for r in got[2])       # the parent (at least) was stopped

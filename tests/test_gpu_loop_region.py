@@ -138,15 +138,18 @@ def test_region_states(shm_name):
         krex.detach()
 
 
-def _sibling(shm_name, q, seconds):
+def _sibling(shm_name, q, seconds, ready):
     import torch as th
     import paper_2609_30057_amd as k
     th.cuda.init()
-    k.attach(shm_name=shm_name)
     n = 1 << 24
     x = th.empty(n, dtype=th.float16, device="cuda")
     y = th.empty_like(x)
     out = k.check_result_buffer()
+    k.gen(x, 2, 0, "uniform", -4.0, 4.0)
+    th.cuda.synchronize()
+    k.attach(shm_name=shm_name)                  # registered once initialised (stopped only after this)
+    ready.set()
     end = time.monotonic() + seconds
     results = set()
     rounds = 0
@@ -160,9 +163,11 @@ def _sibling(shm_name, q, seconds):
     k.detach()
 
 
-def test_two_processes_share_gpu_invariant_results(shm_name):
+@pytest.mark.parametrize("cpu_exclusive", [False, True], ids=["gated", "cpu_exclusive"])
+def test_two_processes_share_gpu_invariant_results(shm_name, cpu_exclusive):
     """A sibling loops gen -> inject -> check while this process holds
-    regions; every sibling round gives the solo result."""
+    regions (with CPU exclusivity: the sibling is stopped inside them); every
+    sibling round gives the solo result."""
     n = 1 << 24
     x = torch.empty(n, dtype=torch.float16, device="cuda")
     y = torch.empty_like(x)
@@ -172,14 +177,18 @@ def test_two_processes_share_gpu_invariant_results(shm_name):
     solo_key = (solo.mismatches, solo.argmax_abs, solo.max_abs, solo.max_rel, int(x[12345].view(torch.int16)))
     ctx = mp.get_context("spawn")
     q = ctx.Queue()
-    p = ctx.Process(target=_sibling, args=(shm_name, q, 4.0))
+    ready = ctx.Event()
+    p = ctx.Process(target=_sibling, args=(shm_name, q, 4.0, ready))
     p.start()
-    krex.attach(shm_name=shm_name)
+    krex.attach(shm_name=shm_name, cpu_exclusive=cpu_exclusive)
+    frozen = []
     try:
         sink = torch.empty(krex.PROBE_THREADS, dtype=torch.float32, device="cuda")
-        time.sleep(1.0)
+        assert ready.wait(120)
+        time.sleep(0.3)
         for _ in range(10):
             krex.time_loop(krex.probe_launcher(20000, sink), 1, 3, region=True)
+            frozen.append(krex.gate_stats()["last_frozen"])
             time.sleep(0.05)
         drains = krex.gate_stats()
     finally:
@@ -189,3 +198,4 @@ def test_two_processes_share_gpu_invariant_results(shm_name):
     assert p.exitcode == 0
     assert rounds > 3 and results == [solo_key]
     assert drains["regions"] == 10
+    assert frozen == ([1] * 10 if cpu_exclusive else [0] * 10)
