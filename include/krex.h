@@ -101,7 +101,7 @@ typedef struct krex_check_result {
  * stops the process tree of every other registered process with SIGSTOP and
  * pins the entering thread to one core of its affinity set (the core named
  * by the KREX_REGION_CPU environment variable if it is in the set, else the
- * highest-numbered one); region exit resumes them with SIGCONT and restores
+ * highest-numbered one; KREX_REGION_CPU=none disables the pinning); region exit resumes them with SIGCONT and restores
  * the affinity before the gate reopens. A holder that dies inside such a
  * region has its stopped siblings resumed by the process that recovers the
  * lock. Returns KREX_EINVAL for unknown flags, KREX_ESTATE if already

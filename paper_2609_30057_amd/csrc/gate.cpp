@@ -620,10 +620,13 @@ int region_begin(uint32_t timeout_ms)
             frozen += (uint64_t)freeze_tree(pid, self, until);
         }
         s.last_frozen.store(frozen);
-        // Step 5 (second half): pin this thread to one core of its set.
-        if (sched_getaffinity(0, sizeof(cpu_set_t), &s.saved_affinity) == 0) {
+        // Step 5 (second half): pin this thread to one core of its set
+        // (KREX_REGION_CPU=none leaves it unpinned).
+        const char *pin_env = getenv("KREX_REGION_CPU");
+        const bool pin = !(pin_env && strcmp(pin_env, "none") == 0);
+        if (pin && sched_getaffinity(0, sizeof(cpu_set_t), &s.saved_affinity) == 0) {
             int core = -1;
-            if (const char *e = getenv("KREX_REGION_CPU")) core = atoi(e);
+            if (pin_env) core = atoi(pin_env);
             if (core < 0 || !CPU_ISSET(core, &s.saved_affinity))
                 for (int c = CPU_SETSIZE - 1; c >= 0; --c)
                     if (CPU_ISSET(c, &s.saved_affinity)) {

@@ -423,7 +423,7 @@ hipError_t launch_inject(void *y, const void *x, int dt, uint64_t n, uint64_t ms
 
 static constexpr uint64_t kIdxMask = (1ull << 33) - 1;   // n < 2^33
 static constexpr int kMaxCheckBlocks = 4096;
-static constexpr int kFinalThreads = 1024;
+static constexpr int kFinalThreads = 256;
 
 struct CheckPartial {
     uint64_t mism;
@@ -444,30 +444,55 @@ struct LaneAcc {
 
 __device__ __forceinline__ uint32_t popc(uint64_t m) { return (uint32_t)__builtin_popcountll(m); }
 
-// One element: counts, ratio candidate; returns d (0 when equal, NaN when
-// unordered) for the |a - b| maximum.
-__device__ __forceinline__ float check_elem(float A, float B, float rtol, float atol, LaneAcc &acc)
+// Every d > 0 has d / |b| >= 2^-26 (fp32 operands that differ are at least
+// one spacing of the nearer one apart, or |b| / 2 when far apart; b = 0 gives
+// +inf), so 2^-32 is a lower bound of any ratio that can raise a maximum
+// above its initial 0.
+static constexpr float kRatioFloor = 0x1p-32f;
+
+// Exact ratio update of one element: the pair (d, bn) replaces (rd, rb) when
+// d / bn > rd / rb, compared as d rb > rd bn in fp64 (products of two fp32
+// values are exact there). An infinite d enters as (inf, 0), ratio +inf, which no
+// later pair exceeds; d = 0 and NaN never compare greater.
+__device__ __forceinline__ void ratio_update(float A, float B, LaneAcc &acc)
 {
     const float d0 = __builtin_fabsf(A - B);
-    const float ab = __builtin_fabsf(B);
-    const bool unord = __builtin_isunordered(A, B);
-    const bool eq = (A == B);
-    // d0 is +inf exactly when the operands differ and one is infinite, or
-    // their difference overflows: never close, ratio +inf.
     const bool dinf = d0 == __builtin_inff();
-    const float rt = rtol * ab;
-    const float thr = atol + rt;
-    // Non-short-circuit operators keep every predicate a lane mask (no branch).
-    const bool close = eq | ((d0 <= thr) & !dinf);
-    acc.wmism += popc(__ballot(!close));
-    acc.wnan += popc(__ballot(unord));
-    // Ratio candidate (d0, bn); an infinite d0 enters as (inf, 0), ratio +inf,
-    // which no later pair exceeds. d0 = 0 and NaN never compare greater.
-    const float bn = dinf ? 0.0f : ab;
+    const float bn = dinf ? 0.0f : __builtin_fabsf(B);
     const bool greater = (double)d0 * (double)acc.rb > (double)acc.rd * (double)bn;
     acc.rd = greater ? d0 : acc.rd;
     acc.rb = greater ? bn : acc.rb;
-    return eq ? 0.0f : d0;
+}
+
+// Counts and verdict of one element, accumulated as wave ballots of plain
+// comparisons (each lowers to one compare writing a lane mask). The element
+// mismatches when a != b (unordered included) and not d0 <= min(thr,
+// FLT_MAX): d0 is +inf exactly when the operands differ and one is infinite,
+// or their difference overflows, and is then never close; clamping the
+// threshold to the largest float excludes it in the same comparison (a NaN
+// threshold, 0 x inf, arises only with |b| = inf, where d0 is inf or NaN and
+// the verdict is a mismatch either way).
+__device__ __forceinline__ uint64_t count_elem(float A, float B, float d0, float ab, float rtol, float atol,
+                                               LaneAcc &acc)
+{
+    const float rt = rtol * ab;
+    const float thr = __builtin_fminf(atol + rt, 0x1.fffffep127f);
+    const uint64_t ne = __ballot(A != B);
+    const uint64_t far = __ballot(!(d0 <= thr));
+    const uint64_t unord = __ballot(__builtin_isunordered(A, B));
+    acc.wmism += popc(ne & far);
+    acc.wnan += popc(unord);
+    return ne & ~unord;             // lanes whose operands are ordered and differ
+}
+
+// One element with its exact ratio update; returns d (0 when equal, NaN when
+// unordered) for the |a - b| maximum. Used for the n mod E tail.
+__device__ __forceinline__ float check_elem(float A, float B, float rtol, float atol, LaneAcc &acc)
+{
+    const float d0 = __builtin_fabsf(A - B);
+    count_elem(A, B, d0, __builtin_fabsf(B), rtol, atol, acc);
+    ratio_update(A, B, acc);
+    return (A == B) ? 0.0f : d0;
 }
 
 // The same d, for re-reading the best chunk.
@@ -490,10 +515,12 @@ struct ChunkIO {
     struct Raw {
         union {
             uint4 v[VA];
+            uint32_t w[4 * VA];
             TA s[E];
         } a;
         union {
             uint4 v[VB];
+            uint32_t w[4 * VB];
             TB s[E];
         } b;
     };
@@ -506,13 +533,33 @@ struct ChunkIO {
         for (int i = 0; i < VB; ++i) r.b.v[i] = reinterpret_cast<const uint4 *>(b)[c * VB + i];
     }
 
+    // fp8 elements are converted two at a time straight from their 32-bit
+    // words (the packed converter's half-word select: no shifts or masks).
+    template <int DT, int NW>
+    __device__ __forceinline__ static void widen_words(const uint32_t (&w)[NW],
+                                                       const typename dtype_traits<DT>::storage (&s)[E], float (&X)[E])
+    {
+        if constexpr (DT == F8) {
+            typedef float f2 __attribute__((ext_vector_type(2)));
+#pragma unroll
+            for (int i = 0; i < NW; ++i) {
+                const f2 lo = __builtin_amdgcn_cvt_pk_f32_fp8((int)w[i], false);
+                const f2 hi = __builtin_amdgcn_cvt_pk_f32_fp8((int)w[i], true);
+                X[4 * i + 0] = lo.x;
+                X[4 * i + 1] = lo.y;
+                X[4 * i + 2] = hi.x;
+                X[4 * i + 3] = hi.y;
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < E; ++e) X[e] = widen<DT>(s[e]);
+        }
+    }
+
     __device__ __forceinline__ static void widen_raw(const Raw &r, float (&A)[E], float (&B)[E])
     {
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-            A[e] = widen<DA>(r.a.s[e]);
-            B[e] = widen<DB>(r.b.s[e]);
-        }
+        widen_words<DA, 4 * VA>(r.a.w, r.a.s, A);
+        widen_words<DB, 4 * VB>(r.b.w, r.b.s, B);
     }
 
     __device__ __forceinline__ static void load(const uint8_t *a, const uint8_t *b, uint64_t c, float (&A)[E],
@@ -532,6 +579,38 @@ struct ChunkIO {
     }
 };
 
+// max_rel with a wave-wide filter: R (wave-uniform) is a lower bound of the
+// largest exact ratio the wave holds. An element whose ratio is at least R
+// has d >= R |b| exactly, hence d >= fl(R |b|) (rounding is monotone and d
+// is a float); so an element with d < fl(R |b|) cannot raise the maximum and
+// skips the exact fp64 update. Only when some lane of the wave has a
+// candidate does the wave run the exact updates for the chunk and raise R to
+// the wave maximum of one-ulp-lowered fl(rd / rb). Only ordered, differing
+// elements are candidates; a NaN product (inf x 0) counts as one. Called by
+// every lane of the wave (the shuffles read
+// all lanes) with the wave's candidate mask; lanes without a chunk pass
+// valid = false.
+template <int E>
+struct RatioFilter {
+    float R = kRatioFloor;
+
+    __device__ __forceinline__ void chunk(const float (&A)[E], const float (&B)[E], bool valid, uint64_t cand,
+                                          LaneAcc &acc)
+    {
+        if (cand == 0) return;                  // wave-uniform
+        if (valid) {
+#pragma unroll
+            for (int e = 0; e < E; ++e) ratio_update(A[e], B[e], acc);
+        }
+        const float q = acc.rd / acc.rb;        // 0, a positive float, or +inf
+        float lo = (q > 0.0f && q < __builtin_inff()) ? __uint_as_float(__float_as_uint(q) - 1u) : q;
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) lo = __builtin_fmaxf(lo, __shfl_xor(lo, off, 64));
+        lo = __uint_as_float(__builtin_amdgcn_readfirstlane(__float_as_uint(lo)));
+        R = __builtin_fmaxf(R, lo);
+    }
+};
+
 template <int DA, int DB, bool VEC>
 __global__ __launch_bounds__(kThreads) void k_check(const uint8_t *a, const uint8_t *b, uint64_t n, float rtol,
                                                     float atol, CheckPartial *partials, uint32_t U)
@@ -542,46 +621,78 @@ __global__ __launch_bounds__(kThreads) void k_check(const uint8_t *a, const uint
     const uint64_t nchunks = n / E;
     const uint64_t base = (uint64_t)blockIdx.x * kThreads * U;
     LaneAcc acc{0u, 0u, 0.0f, 1.0f};
+    RatioFilter<E> rf;
     float best_d = -1.0f;               // largest non-NaN d seen by this lane
     uint32_t best_c = 0;                // its chunk
-    auto process = [&](const float (&A)[E], const float (&B)[E], uint64_t c) {
-        float cmax = -1.0f;   // NaN d (unordered) is ignored by the maximum
+    // Counts and |a - b| maximum of one chunk; returns the lanes of the wave
+    // whose chunk has a max_rel candidate.
+    auto process = [&](const float (&A)[E], const float (&B)[E], uint64_t c) -> uint64_t {
+        float cmax = -1.0f;             // NaN d (unordered) is ignored by the maximum
+        uint64_t cand = 0;
 #pragma unroll
-        for (int e = 0; e < E; ++e) cmax = __builtin_fmaxf(cmax, check_elem(A[e], B[e], rtol, atol, acc));
+        for (int e = 0; e < E; ++e) {
+            const float d0 = __builtin_fabsf(A[e] - B[e]);
+            const float ab = __builtin_fabsf(B[e]);
+            const uint64_t differ = count_elem(A[e], B[e], d0, ab, rtol, atol, acc);
+            // Equal operands (ratio 0, or 0/0) and unordered ones (NaN d)
+            // never raise the maximum: only ordered, differing elements are
+            // candidates (otherwise every zero reference would be one).
+            cand |= __ballot(!(d0 < rf.R * ab)) & differ;
+            cmax = __builtin_fmaxf(cmax, (A[e] == B[e]) ? 0.0f : d0);
+        }
         if (cmax > best_d) {
             best_d = cmax;
             best_c = (uint32_t)c;
         }
+        return cand;
     };
     if constexpr (VEC) {
-        // Software pipeline: the next chunk's loads are in flight while the
-        // current one is evaluated. A lane's chunks only grow with u, so the
-        // first lane of a wave is active whenever any lane is.
-        typename IO::Raw cur, nxt;
-        uint64_t c = base + t;
-        bool have = c < nchunks;
-        if (have) IO::load_raw(a, b, c, cur);
-        for (uint32_t u = 0; u < U; ++u) {
-            const uint64_t cn = c + kThreads;
-            const bool have_n = (u + 1 < U) && cn < nchunks;
-            if (have_n) IO::load_raw(a, b, cn, nxt);
-            if (have) {
-                float A[E], B[E];
-                IO::widen_raw(cur, A, B);
-                process(A, B, c);
+        // Software pipeline over two chunk buffers: the loads of the next
+        // chunk are in flight while the current one is evaluated. Every load
+        // is unconditional (a lane with nothing left re-reads its current
+        // chunk, or the last one), so the compiler's memory-counter waits
+        // stay exact: an evaluation waits for its own buffer only, never for
+        // the loads just issued. A lane's chunks only grow with u, so the
+        // first lane of a wave holds a chunk whenever any lane does.
+        if (nchunks != 0) {
+            const uint64_t last = nchunks - 1;
+            auto step = [&](const typename IO::Raw &r, bool h, uint64_t c) {
+                float A[E], B[E];       // read only where h holds
+                uint64_t cand = 0;
+                if (h) {
+                    IO::widen_raw(r, A, B);
+                    cand = process(A, B, c);
+                }
+                rf.chunk(A, B, h, cand, acc);
+            };
+            typename IO::Raw r0, r1;
+            uint64_t c0 = base + t;
+            bool h0 = c0 < nchunks;
+            IO::load_raw(a, b, h0 ? c0 : last, r0);
+            for (uint32_t u = 0; u < U; u += 2) {
+                const uint64_t c1 = c0 + kThreads;
+                const bool h1 = (u + 1 < U) && c1 < nchunks;
+                IO::load_raw(a, b, h1 ? c1 : (h0 ? c0 : last), r1);
+                step(r0, h0, c0);
+                const uint64_t c2 = c1 + kThreads;
+                const bool h2 = (u + 2 < U) && c2 < nchunks;
+                IO::load_raw(a, b, h2 ? c2 : (h1 ? c1 : last), r0);
+                step(r1, h1, c1);
+                c0 = c2;
+                h0 = h2;
             }
-            cur = nxt;
-            c = cn;
-            have = have_n;
         }
     } else {
         for (uint32_t u = 0; u < U; ++u) {
             const uint64_t c = base + (uint64_t)u * kThreads + t;
-            if (c < nchunks) {
-                float A[E], B[E];
+            const bool have = c < nchunks;
+            float A[E], B[E];           // read only where have holds
+            uint64_t cand = 0;
+            if (have) {
                 IO::load(a, b, c, A, B);
-                process(A, B, c);
+                cand = process(A, B, c);
             }
+            rf.chunk(A, B, have, cand, acc);
         }
     }
     // First element of the lane's best chunk attaining best_d.
@@ -647,6 +758,8 @@ __global__ __launch_bounds__(kThreads) void k_check(const uint8_t *a, const uint
 __global__ __launch_bounds__(kFinalThreads) void k_check_final(const CheckPartial *partials, uint32_t nblocks,
                                                                uint64_t n, krex_check_result *out)
 {
+    // Every thread issues all of its partial loads before using any, so the
+    // kernel pays one memory latency.
     constexpr int PER = kMaxCheckBlocks / kFinalThreads;
     uint64_t m = 0, nn = 0, key = 0;
     uint32_t rb = 0;
@@ -673,8 +786,9 @@ __global__ __launch_bounds__(kFinalThreads) void k_check_final(const CheckPartia
         const uint32_t r2 = __shfl_xor(rb, off, 64);
         rb = r2 > rb ? r2 : rb;
     }
-    __shared__ uint64_t s_m[kFinalThreads / 64], s_n[kFinalThreads / 64], s_k[kFinalThreads / 64];
-    __shared__ uint32_t s_r[kFinalThreads / 64];
+    constexpr int W = kFinalThreads / 64;
+    __shared__ uint64_t s_m[W], s_n[W], s_k[W];
+    __shared__ uint32_t s_r[W];
     const int w = threadIdx.x / 64;
     if ((threadIdx.x & 63) == 0) {
         s_m[w] = m;
@@ -684,7 +798,8 @@ __global__ __launch_bounds__(kFinalThreads) void k_check_final(const CheckPartia
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-        for (int i = 1; i < kFinalThreads / 64; ++i) {
+#pragma unroll
+        for (int i = 1; i < W; ++i) {
             s_m[0] += s_m[i];
             s_n[0] += s_n[i];
             s_k[0] = s_k[i] > s_k[0] ? s_k[i] : s_k[0];
@@ -703,6 +818,27 @@ __global__ __launch_bounds__(kFinalThreads) void k_check_final(const CheckPartia
     }
 }
 
+// Blocks of k_check<DA, DB, VEC> the current device holds at once, capped at
+// the partial buffer's capacity; cached per device.
+template <int DA, int DB, bool VEC>
+static uint32_t check_resident()
+{
+    constexpr int kDevCache = 64;
+    static uint32_t cache[kDevCache] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kDevCache) dev = -1;
+    if (dev >= 0 && cache[dev]) return cache[dev];
+    int per_cu = 0, cus = 0;
+    uint32_t r = kMaxCheckBlocks / 2;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_check<DA, DB, VEC>, kThreads, 0) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev < 0 ? 0 : dev) == hipSuccess &&
+        per_cu > 0 && cus > 0)
+        r = (uint32_t)per_cu * (uint32_t)cus;
+    if (r > (uint32_t)kMaxCheckBlocks) r = kMaxCheckBlocks;
+    if (dev >= 0) cache[dev] = r;
+    return r;
+}
+
 template <int DA, int DB>
 static hipError_t check_ab(const void *a, const void *b, uint64_t n, float rtol, float atol, void *scratch,
                            krex_check_result *out, hipStream_t s)
@@ -711,11 +847,15 @@ static hipError_t check_ab(const void *a, const void *b, uint64_t n, float rtol,
     constexpr int E = 16 / (SA < SB ? SA : SB);
     const bool vec = (((uintptr_t)a & 15u) == 0 && ((uintptr_t)b & 15u) == 0);
     const uint64_t nchunks = n / E;
-    // Chunks per thread: enough that the grid stays within the partial
-    // buffer, and at least 8 so that the per-lane re-read of the best chunk
-    // adds at most 1/8 to the bytes read (and the pipeline has depth).
+    // One resident round: the grid is at most the number of blocks the
+    // device holds at once (occupancy x compute units), so no partial last
+    // round of blocks idles most of the chip. Chunks per thread: enough to
+    // cover n with that grid, and at least 8 so that the per-lane re-read of
+    // the best chunk adds at most 1/8 to the bytes read (and the pipeline
+    // has depth).
     static const uint32_t u_floor = tune_env("KREX_CHECK_U", 8);
-    uint64_t U = (nchunks + (uint64_t)kThreads * kMaxCheckBlocks - 1) / ((uint64_t)kThreads * kMaxCheckBlocks);
+    const uint64_t resident = vec ? check_resident<DA, DB, true>() : check_resident<DA, DB, false>();
+    uint64_t U = (nchunks + (uint64_t)kThreads * resident - 1) / ((uint64_t)kThreads * resident);
     if (U < u_floor) U = u_floor;
     if (U == 0) U = 1;
     uint64_t G = (nchunks + (uint64_t)kThreads * U - 1) / ((uint64_t)kThreads * U);

@@ -39,7 +39,8 @@ struct words4 {
 // two 32x32->64 products M0*x0 and M1*x2 are formed and the state becomes
 // (hi(M1 x2) ^ x1 ^ k0, lo(M1 x2), hi(M0 x0) ^ x3 ^ k1, lo(M0 x0)); the key
 // advances by the Weyl constants between rounds. The key is wave-uniform,
-// so its schedule lives in scalar registers.
+// so its schedule lives in scalar registers. Each three-way xor is one
+// gfx950 v_bitop3_b32 (truth table 0x96: odd parity of the three inputs).
 __device__ __forceinline__ words4 philox10(uint32_t c0, uint32_t c1, uint32_t k0, uint32_t k1)
 {
     uint32_t x0 = c0, x1 = c1, x2 = 0u, x3 = 0u;
@@ -47,9 +48,9 @@ __device__ __forceinline__ words4 philox10(uint32_t c0, uint32_t c1, uint32_t k0
     for (int r = 0; r < 10; ++r) {
         const uint64_t p0 = (uint64_t)0xD2511F53u * (uint64_t)x0;
         const uint64_t p1 = (uint64_t)0xCD9E8D57u * (uint64_t)x2;
-        const uint32_t n0 = (uint32_t)(p1 >> 32) ^ x1 ^ k0;
+        const uint32_t n0 = __builtin_amdgcn_bitop3_b32((uint32_t)(p1 >> 32), x1, k0, 0x96);
         const uint32_t n1 = (uint32_t)p1;
-        const uint32_t n2 = (uint32_t)(p0 >> 32) ^ x3 ^ k1;
+        const uint32_t n2 = __builtin_amdgcn_bitop3_b32((uint32_t)(p0 >> 32), x3, k1, 0x96);
         const uint32_t n3 = (uint32_t)p0;
         x0 = n0; x1 = n1; x2 = n2; x3 = n3;
         k0 += 0x9E3779B9u;

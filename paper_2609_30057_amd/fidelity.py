@@ -19,10 +19,11 @@ Procedure, on one GPU:
      nothing excludes the siblings from the timed interval;
   6. frozen (optional): gated, and the holder's regions also stop the
      siblings' process trees and pin the timing thread (CPU exclusivity,
-     Section 4.2 steps 4, 5 and 7).
+     Section 4.2 steps 4, 5 and 7); frozen_nopin stops them without pinning.
 t_native is the median of the native run per duration.
 """
 import multiprocessing as mp
+import os
 import sys
 import time
 import uuid
@@ -105,7 +106,12 @@ def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, mode
     for mode in ["native"] + compared:
         gated = mode != "ungated"
         shm = "/krex-fid-%s" % uuid.uuid4().hex[:10]
-        krex.attach(0, shm_name=shm, gated=gated, cpu_exclusive=(mode == "frozen"))
+        frozen = mode in ("frozen", "frozen_nopin")
+        if mode == "frozen_nopin":
+            os.environ["KREX_REGION_CPU"] = "none"
+        else:
+            os.environ.pop("KREX_REGION_CPU", None)
+        krex.attach(0, shm_name=shm, gated=gated, cpu_exclusive=frozen)
         if mode == "native":
             plan = []
             for d in durations_ms:
@@ -113,7 +119,7 @@ def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, mode
                 plan.append((d, iters))
                 result["calibrated"][str(d)] = {"iters": iters, "ms": round(t, 4)}
         procs, stop, q = [], ctx.Event(), ctx.Queue()
-        if mode in ("gated", "ungated", "frozen"):
+        if mode in ("gated", "ungated", "frozen", "frozen_nopin"):
             readies = []
             for _ in range(siblings):
                 ready = ctx.Event()
@@ -156,4 +162,7 @@ def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, mode
         result["within_5pct"][key] = {m: round(stats.within(times[m][d], native), 4)
                                       for m in compared}
         result["calibrated"][key]["native_median_ms"] = round(native, 4)
+        result.setdefault("ratio_quantiles", {})[key] = {
+            m: [round(float(q), 4) for q in np.percentile(np.asarray(times[m][d]) / native, [5, 50, 90, 95, 99, 100])]
+            for m in ["native"] + compared}
     return result

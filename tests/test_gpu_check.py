@@ -104,3 +104,46 @@ def test_identical_large_inputs():
     krex.gen(x, 3, 0, "uniform", -4.0, 4.0)
     r = krex.check(x, x, 0.0, 0.0)
     assert (r.mismatches, r.nan_count, r.argmax_abs, r.max_abs, r.max_rel) == (0, 0, 0, 0.0, 0.0)
+
+
+def _ratio_inputs(kind, n, seed):
+    """fp32 (a, b) pairs stressing the max_rel search: ratios rising or
+    falling along the tensor, near-ties within one ulp of the ratio, tiny and
+    subnormal references, b = 0 and an infinite difference placed late."""
+    rng = np.random.default_rng(seed)
+    b = rng.uniform(1.0, 2.0, n).astype(np.float32)
+    if kind == "rising":
+        r = np.linspace(1e-3, 2e-3, n, dtype=np.float64)
+    elif kind == "falling":
+        r = np.linspace(2e-3, 1e-3, n, dtype=np.float64)
+    elif kind == "ties":
+        r = np.full(n, 1e-3)
+    else:
+        r = rng.uniform(0.0, 1e-3, n)
+    d = (r * b).astype(np.float32)
+    a = (b + d).astype(np.float32)
+    if kind == "subnormal":
+        b[::3] = (b[::3] * np.float32(2.0 ** -140)).astype(np.float32)   # subnormal references
+        a[::3] = (b[::3] * np.float32(1.5)).astype(np.float32)
+    if kind == "late_specials":
+        b[n - 5] = 0.0
+        a[n - 5] = 1e-30
+        a[n - 2] = np.float32(3e38)
+        b[n - 2] = np.float32(-3e38)                             # difference overflows: ratio +inf
+    return a, b
+
+
+@pytest.mark.parametrize("kind", ["rising", "falling", "ties", "random", "subnormal", "late_specials"])
+def test_max_rel_search_matches_oracle(kind):
+    """max_rel at 0 ULP where the wave filter of the kernel is exercised hard:
+    every chunk raising the maximum, maxima only at the start, exact ratios
+    equal to within an ulp across lanes and waves, subnormal references, and
+    an infinite ratio in the n mod E tail or just before it."""
+    for n in (1003, (1 << 20) + 5):
+        a, b = _ratio_inputs(kind, n, 5)
+        for dta, dtb in (("f32", "f32"), ("f16", "f32"), ("bf16", "bf16"), ("f8", "f16")):
+            ac = oracle.from_f32(a, dta) if dta != "f32" else a
+            bc = oracle.from_f32(b, dtb) if dtb != "f32" else b
+            ref = oracle.check(ac, dta, bc, dtb, 1e-3, 1e-5)
+            r = krex.check(from_storage(ac, dta), from_storage(bc, dtb), 1e-3, 1e-5)
+            same_result(r, ref)
