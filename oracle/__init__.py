@@ -58,6 +58,9 @@ def lib():
         L.ko_gen.argtypes = [vp, ctypes.c_int, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64,
                              ctypes.c_int, ctypes.c_float, ctypes.c_float]
         L.ko_gen.restype = ctypes.c_int
+        L.ko_gen_packed.argtypes = [vp, ctypes.c_int, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64,
+                                    ctypes.c_int, ctypes.c_float, ctypes.c_float]
+        L.ko_packed_width.argtypes = [ctypes.c_int, ctypes.c_int]
         L.ko_transform_words.argtypes = [vp, ctypes.c_int, ctypes.c_uint64, vp, ctypes.c_int,
                                          ctypes.c_float, ctypes.c_float]
         L.ko_transform_words.restype = ctypes.c_int
@@ -124,6 +127,21 @@ def gen(dt, n, seed, offset=0, dist=UNIFORM, p0=-1.0, p1=1.0):
     st = lib().ko_gen(_ptr(out), dt, n, seed, offset, dist, p0, p1)
     if st != 0:
         raise ValueError("ko_gen rejected its arguments (%d)" % st)
+    return out
+
+
+def packed_width(dt, dist):
+    """Field width in bits of the packed stream for (dtype, distribution); 0 if none."""
+    return int(lib().ko_packed_width(dtype_code(dt), dist))
+
+
+def gen_packed(dt, n, seed, offset=0, dist=UNIFORM, p0=-1.0, p1=1.0):
+    """Packed-stream tensor (narrow dtypes only) as its storage array; offset counts fields."""
+    dt = dtype_code(dt)
+    out = np.empty(n, dtype=NP_STORAGE[dt])
+    st = lib().ko_gen_packed(_ptr(out), dt, n, seed, offset, dist, p0, p1)
+    if st != 0:
+        raise ValueError("ko_gen_packed rejected its arguments (%d)" % st)
     return out
 
 

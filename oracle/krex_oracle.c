@@ -473,6 +473,79 @@ int ko_gen(void *dst, int dt, uint64_t n, uint64_t seed, uint64_t offset,
     return KO_OK;
 }
 
+/* ------------------------------------------------------------------------
+ * Packed stream: the narrow-dtype form of the generator, which spends w < 32
+ * bits of the word stream per element. The stream is cut into w-bit fields,
+ * low bits first: field q is bits [(q mod k) w, (q mod k) w + w) of word
+ * W_s[q / k], k = 32 / w. w = 16 for bf16 and fp16 (every distribution)
+ * and for fp8 normal; w = 8 for fp8 uniform and bitcast; fp32 and u32 have
+ * no packed form. Element j of a tensor generated at field offset o uses
+ * field q = o + j:
+ *   uniform  the uniform transform above of the word f << (32 - w), i.e.
+ *            u = f 2^-w;
+ *   normal   the Box-Muller transform above of the word pair
+ *            (f_{2p} << 16, f_{2p+1} << 16), p = q >> 1 (both fields lie in
+ *            word p), the cosine branch for even q, the sine branch for odd
+ *            q; v = mu + sigma z;
+ *   bitcast  the element's bits are the field itself.
+ * ---------------------------------------------------------------------- */
+int ko_packed_width(int dt, int dist)
+{
+    if (dist != KO_UNIFORM && dist != KO_NORMAL && dist != KO_BITCAST)
+        return 0;
+    if (dt == KO_BF16 || dt == KO_F16)
+        return 16;
+    if (dt == KO_F8E4M3)
+        return dist == KO_NORMAL ? 16 : 8;
+    return 0;
+}
+
+/* Field q of the stream of seed. */
+static uint32_t packed_field(uint64_t seed, uint64_t q, int w)
+{
+    uint64_t k = 32u / (unsigned)w;
+    uint32_t W = ko_word(seed, q / k);
+    uint32_t shift = (uint32_t)(q % k) * (uint32_t)w;
+    uint32_t mask = (w == 32) ? 0xFFFFFFFFu : ((1u << w) - 1u);
+    return (W >> shift) & mask;
+}
+
+int ko_gen_packed(void *dst, int dt, uint64_t n, uint64_t seed, uint64_t offset,
+                  int dist, float p0, float p1)
+{
+    int w = ko_packed_width(dt, dist);
+    if (w == 0 || !params_ok(dist, p0, p1))
+        return KO_EINVAL;
+    if (n > 0 && offset > UINT64_MAX - (n - 1))
+        return KO_EINVAL;
+    for (uint64_t j = 0; j < n; ++j) {
+        uint64_t q = offset + j;
+        uint32_t f = packed_field(seed, q, w);
+        if (dist == KO_BITCAST) {
+            if (w == 16)
+                ((uint16_t *)dst)[j] = (uint16_t)f;
+            else
+                ((uint8_t *)dst)[j] = (uint8_t)f;
+            continue;
+        }
+        float v;
+        if (dist == KO_UNIFORM) {
+            v = ko_uniform(f << (32 - w), p0, p1);
+        } else {
+            uint64_t qp = q & ~(uint64_t)1;  /* first field of the pair */
+            uint32_t fa = packed_field(seed, qp, w);
+            uint32_t fb = packed_field(seed, qp + 1, w);
+            float z0, z1;
+            ko_normal_pair(fa << 16, fb << 16, &z0, &z1);
+            float z = (q & 1u) ? z1 : z0;
+            float sz = p1 * z;
+            v = p0 + sz;
+        }
+        store_f32(dst, dt, j, v);
+    }
+    return KO_OK;
+}
+
 /* The same transforms on caller-supplied words: element j uses words[j];
  * the normal pair of element j is (words[j & ~1], words[j | 1]). */
 int ko_transform_words(void *dst, int dt, uint64_t n, const uint32_t *words,
