@@ -258,6 +258,11 @@ def run_kernels():
     rec("gen f32 normal 16.8M", t_ms(lambda: krex.gen(b_f32, 1, 0, "normal")), N * 4)
     rec("gen f32 uniform 67M", t_ms(lambda: krex.gen(xf, 7, 0)), xf.numel() * 4)
     rec("gen f8 normal 268M", t_ms(lambda: krex.gen(x8, 5, 0, "normal")), x8.numel())
+    rec("gen packed f16 uniform 268M", t_ms(lambda: krex.gen_packed(x16, 2, 0, "uniform", -4.0, 4.0)),
+        x16.numel() * 2)
+    rec("gen packed bf16 normal 16.8M", t_ms(lambda: krex.gen_packed(a_bf, 1, 0, "normal")), N * 2)
+    rec("gen packed f8 uniform 268M", t_ms(lambda: krex.gen_packed(x8, 5, 0, "uniform", -4.0, 4.0)), x8.numel())
+    rec("gen packed f8 normal 268M", t_ms(lambda: krex.gen_packed(x8, 5, 0, "normal")), x8.numel())
     rec("inject f16 exact 268M", t_ms(lambda: krex.inject(y16, x16, 3, 0.001, 0.5)), x16.numel() * 4)
     krex.inject(y8, x8, 6, 0.01, 0.25, "round")
     krex.inject(yf, xf, 8, 0.01, 0.5)

@@ -132,6 +132,23 @@ krex_status krex_detach(void);
 krex_status krex_gen(void *dst, int32_t dtype, uint64_t n, uint64_t seed, uint64_t offset,
                      int32_t dist, float p0, float p1, void *stream);
 
+/* Packed stream, the narrow-dtype form of krex_gen (same Philox words,
+ * fewer per element; an extension of the generation of Section 1 and
+ * Section 2.1, which name no generator). The word stream is cut into W-bit
+ * fields, low bits first: field q is bits [(q mod K) W, (q mod K) W + W) of
+ * W_seed[q / K], K = 32 / W. W = 16 for KREX_BF16 and KREX_F16 (every
+ * distribution) and for KREX_F8E4M3 with KREX_NORMAL; W = 8 for KREX_F8E4M3
+ * uniform and bitcast. Element j uses field q = offset + j (offset counts
+ * fields). Uniform: krex_gen's uniform transform of the word f << (32 - W),
+ * i.e. u = f 2^-W. Normal: krex_gen's Box-Muller on the word pair
+ * (f_{2p} << 16, f_{2p+1} << 16), p = q >> 1 (both fields in word p), cosine
+ * branch for even q, sine for odd. Bitcast: the element's bits are the
+ * field. Rounding and parameter rules as krex_gen. dst: device, aligned to
+ * the element size; fastest when 16-byte aligned with offset a multiple of
+ * 16 / element size. KREX_EINVAL for KREX_F32 or KREX_U32. */
+krex_status krex_gen_packed(void *dst, int32_t dtype, uint64_t n, uint64_t seed, uint64_t offset,
+                            int32_t dist, float p0, float p1, void *stream);
+
 /* Same transforms applied to caller-supplied words: element j of dst is
  * transform(words[j]) (normal: pairs (words[2p], words[2p + 1]); n even).
  * words: device, n uint32 values. */

@@ -106,6 +106,7 @@ def lib():
             "krex_attach": (i32, [i32, ctypes.c_char_p, u32]),
             "krex_detach": (i32, []),
             "krex_gen": (i32, [vp, i32, u64, u64, u64, i32, f32, f32, vp]),
+            "krex_gen_packed": (i32, [vp, i32, u64, u64, u64, i32, f32, f32, vp]),
             "krex_transform_words": (i32, [vp, i32, u64, vp, i32, f32, f32, vp]),
             "krex_inject": (i32, [vp, vp, i32, u64, u64, u64, f64, f32, i32, vp]),
             "krex_check": (i32, [vp, i32, vp, i32, u64, f32, f32, vp, vp]),
@@ -187,6 +188,20 @@ def gen(t, seed, offset=0, dist="uniform", p0=None, p1=None, stream=None):
         p1 = 1.0 if d == UNIFORM else (1.0 if d == NORMAL else 0.0)
     _chk(lib().krex_gen(_dev(t), dtype_code(t.dtype), t.numel(), seed & (2**64 - 1), offset, d, p0, p1,
                         _stream(stream)), "krex_gen")
+    return t
+
+
+def gen_packed(t, seed, offset=0, dist="uniform", p0=None, p1=None, stream=None):
+    """Packed-stream generation for bf16 / fp16 / fp8 tensors: element j uses
+    the 16- or 8-bit field offset + j of the Philox word stream (bitcast:
+    the field's bits)."""
+    d = _dist(dist)
+    if p0 is None:
+        p0 = -1.0 if d == UNIFORM else 0.0
+    if p1 is None:
+        p1 = 1.0 if d == UNIFORM else (1.0 if d == NORMAL else 0.0)
+    _chk(lib().krex_gen_packed(_dev(t), dtype_code(t.dtype), t.numel(), seed & (2**64 - 1), offset, d, p0, p1,
+                               _stream(stream)), "krex_gen_packed")
     return t
 
 

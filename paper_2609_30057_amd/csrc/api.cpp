@@ -321,6 +321,20 @@ krex_status krex_gen(void *dst, int32_t dtype, uint64_t n, uint64_t seed, uint64
     return submit(s, [&] { return krex::launch_gen(dst, dtype, n, seed, offset, dist, p0, p1, s); });
 }
 
+krex_status krex_gen_packed(void *dst, int32_t dtype, uint64_t n, uint64_t seed, uint64_t offset, int32_t dist,
+                            float p0, float p1, void *stream)
+{
+    if (dtype != KREX_BF16 && dtype != KREX_F16 && dtype != KREX_F8E4M3) return KREX_EINVAL;
+    const size_t es = elem_size(dtype);
+    if (!gen_params_ok(dist, p0, p1)) return KREX_EINVAL;
+    if (n > 0 && offset > UINT64_MAX - (n - 1)) return KREX_EINVAL;
+    if (n > 0 && !dst) return KREX_EINVAL;
+    if (!aligned(dst, es)) return KREX_EALIGN;
+    if (n == 0) return KREX_OK;
+    hipStream_t s = (hipStream_t)stream;
+    return submit(s, [&] { return krex::launch_gen_packed(dst, dtype, n, seed, offset, dist, p0, p1, s); });
+}
+
 krex_status krex_transform_words(void *dst, int32_t dtype, uint64_t n, const uint32_t *words, int32_t dist, float p0,
                                  float p1, void *stream)
 {

@@ -179,6 +179,176 @@ hipError_t launch_gen(void *dst, int dt, uint64_t n, uint64_t seed, uint64_t off
     }
 }
 
+// ------------------------------------------------------------- packed stream
+//
+// The narrow-dtype generator that spends W bits of the word stream per
+// element (W = 16 for bf16 / fp16 and fp8 normal, 8 for fp8 uniform and
+// bitcast): field q is bits (q mod K) W .. of word q / K, K = 32 / W, low
+// bits first; element j uses field offset + j. One thread unit is one
+// 16-byte output vector, E elements = E fields = GB Philox blocks, so every
+// narrow dtype needs one block per 16 bytes (two for fp8 normal) instead of
+// one word per element. Uniform maps field f through the uniform transform
+// of the word f << (32 - W); normal runs Box-Muller on the two 16-bit fields
+// of one word widened to the top half (low field -> cosine, high field ->
+// sine); bitcast stores the fields, i.e. the words' bytes.
+
+template <int DT, int DIST>
+struct packed_of {
+    static constexpr int W = (DT == F8 && DIST != NORMAL) ? 8 : 16;
+    static constexpr int E = 16 / dtype_traits<DT>::size;
+    static constexpr int GB = E * W / 128;
+};
+
+struct PackedParams {
+    uint8_t *dst;
+    uint64_t n;
+    uint64_t offset;   // in fields
+    uint32_t k0, k1;
+    float p0, p1;      // uniform: lo and fl(hi - lo); normal: mean and std
+    float rs;          // uniform: fl(hi - lo) 2^-W when that is exact
+    int scaled;        // rs is exact
+    uint64_t u0;       // first unit (units are E fields, E-aligned)
+    uint64_t nunits;
+    uint32_t U;        // units per thread, block-contiguous
+    int vec;           // offset % E == 0 and dst 16-byte aligned
+};
+
+template <int DT, int DIST>
+__global__ __launch_bounds__(kThreads) void k_gen_packed(PackedParams P)
+{
+    using T = typename dtype_traits<DT>::storage;
+    constexpr int ES = dtype_traits<DT>::size;
+    constexpr int W = packed_of<DT, DIST>::W;
+    constexpr int K = 32 / W;
+    constexpr int E = packed_of<DT, DIST>::E;
+    constexpr int GB = packed_of<DT, DIST>::GB;
+    constexpr uint32_t kMask = (1u << W) - 1u;
+    for (uint32_t u = 0; u < P.U; ++u) {
+        const uint64_t g = ((uint64_t)blockIdx.x * P.U + u) * kThreads + threadIdx.x;
+        if (g >= P.nunits) break;
+        const uint64_t unit = P.u0 + g;
+        uint32_t wv[4 * GB];
+#pragma unroll
+        for (int i = 0; i < GB; ++i) {
+            const words4 w = philox_block(unit * GB + i, P.k0, P.k1);
+#pragma unroll
+            for (int l = 0; l < 4; ++l) wv[4 * i + l] = w.v[l];
+        }
+        union {
+            uint4 v;
+            uint32_t w[4];
+            T s[E];
+        } pk;
+        if constexpr (DIST == BITCAST) {
+            static_assert(GB == 1, "bitcast units are one block");
+#pragma unroll
+            for (int l = 0; l < 4; ++l) pk.w[l] = wv[l];
+        } else if constexpr (DIST == UNIFORM) {
+            float v[E];
+            if (P.scaled) {
+                // u = f 2^-W exactly, and rs = fl(hi - lo) 2^-W exactly, so
+                // the product rs f is the same real number as fl(hi - lo) u
+                // and rounds the same: one conversion, one multiply, one add.
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    const uint32_t f = (wv[e / K] >> ((e % K) * W)) & kMask;
+                    const float t = P.rs * (float)f;
+                    v[e] = P.p0 + t;
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    const uint32_t f = (wv[e / K] >> ((e % K) * W)) & kMask;
+                    v[e] = uniform_f32(f << (32 - W), P.p0, P.p1);
+                }
+            }
+            if constexpr (DT == F8) {
+                // Two values per conversion (bytes 0-1, then 2-3 of the word).
+#pragma unroll
+                for (int i = 0; i < E / 4; ++i) {
+                    uint32_t wd = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(v[4 * i], v[4 * i + 1], 0, false);
+                    wd = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(v[4 * i + 2], v[4 * i + 3], (int)wd, true);
+                    pk.w[i] = wd;
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < E; ++e) pk.s[e] = narrow<DT, false>(v[e]);
+            }
+        } else {
+            static_assert(W == 16, "normal fields are 16 bits");
+#pragma unroll
+            for (int i = 0; i < 4 * GB; ++i) {
+                float z0, z1;
+                normal_pair(wv[i] << 16, wv[i] & 0xFFFF0000u, z0, z1);
+                const float s0 = P.p1 * z0;
+                const float s1 = P.p1 * z1;
+                pk.s[2 * i] = narrow<DT, false>(P.p0 + s0);
+                pk.s[2 * i + 1] = narrow<DT, false>(P.p0 + s1);
+            }
+        }
+        const uint64_t q0 = unit * (uint64_t)E;
+        if (P.vec && q0 >= P.offset && q0 - P.offset + E <= P.n) {
+            *reinterpret_cast<uint4 *>(P.dst + (q0 - P.offset) * ES) = pk.v;
+        } else {
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const uint64_t q = q0 + (uint64_t)e;
+                if (q >= P.offset && q - P.offset < P.n) reinterpret_cast<T *>(P.dst)[q - P.offset] = pk.s[e];
+            }
+        }
+    }
+}
+
+template <int DT, int DIST>
+static hipError_t gen_packed_dt_dist(PackedParams P, hipStream_t s)
+{
+    constexpr int E = packed_of<DT, DIST>::E;
+    constexpr int W = packed_of<DT, DIST>::W;
+    if (DIST == UNIFORM) {
+        P.rs = ldexpf(P.p1, -W);
+        P.scaled = (ldexpf(P.rs, W) == P.p1) ? 1 : 0;
+    } else {
+        P.rs = 0.0f;
+        P.scaled = 0;
+    }
+    P.u0 = P.offset / E;
+    P.nunits = (P.offset + (P.n - 1)) / E - P.u0 + 1;
+    P.vec = (P.offset % E == 0 && ((uintptr_t)P.dst & 15u) == 0) ? 1 : 0;
+    uint32_t grid;
+    shape(P.nunits, 1, &P.U, &grid);
+    return launch(k_gen_packed<DT, DIST>, dim3(grid), dim3(kThreads), s, P);
+}
+
+template <int DT>
+static hipError_t gen_packed_dt(const PackedParams &P, int dist, hipStream_t s)
+{
+    switch (dist) {
+    case UNIFORM: return gen_packed_dt_dist<DT, UNIFORM>(P, s);
+    case NORMAL: return gen_packed_dt_dist<DT, NORMAL>(P, s);
+    default: return gen_packed_dt_dist<DT, BITCAST>(P, s);
+    }
+}
+
+hipError_t launch_gen_packed(void *dst, int dt, uint64_t n, uint64_t seed, uint64_t offset, int dist, float p0,
+                             float p1, hipStream_t s)
+{
+    if (n == 0) return hipSuccess;
+    PackedParams P;
+    P.dst = (uint8_t *)dst;
+    P.n = n;
+    P.offset = offset;
+    P.k0 = (uint32_t)seed;
+    P.k1 = (uint32_t)(seed >> 32);
+    P.p0 = p0;
+    P.p1 = (dist == UNIFORM) ? (p1 - p0) : p1;
+    switch (dt) {
+    case BF16: return gen_packed_dt<BF16>(P, dist, s);
+    case F16: return gen_packed_dt<F16>(P, dist, s);
+    case F8: return gen_packed_dt<F8>(P, dist, s);
+    default: return hipErrorInvalidValue;
+    }
+}
+
 // ------------------------------------------------------------- words transform
 
 struct XformParams {

@@ -16,6 +16,9 @@ int device_cus();
 // `p1` is the distribution's second parameter as given (upper bound or std).
 hipError_t launch_gen(void *dst, int dt, uint64_t n, uint64_t seed, uint64_t offset, int dist, float p0, float p1,
                       hipStream_t s);
+// Packed stream (bf16, fp16, fp8 only); offset counts fields.
+hipError_t launch_gen_packed(void *dst, int dt, uint64_t n, uint64_t seed, uint64_t offset, int dist, float p0,
+                             float p1, hipStream_t s);
 hipError_t launch_xform(void *dst, int dt, uint64_t n, const uint32_t *words, int dist, float p0, float p1,
                         hipStream_t s);
 hipError_t launch_inject(void *y, const void *x, int dt, uint64_t n, uint64_t mseed, uint64_t moff, uint64_t T,

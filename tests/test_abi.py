@@ -69,6 +69,12 @@ def test_host_only_entry_points():
     assert L.krex_gen(ctypes.c_void_p(2), k.F32, 4, 0, 0, 0, -1.0, 1.0, None) == k.EALIGN
     assert L.krex_gen(None, k.F32, 4, 0, 2**64 - 2, 0, -1.0, 1.0, None) == k.EINVAL
     assert L.krex_gen(None, k.F32, 0, 0, 0, 0, 1.0, -1.0, None) == k.EINVAL
+    # the packed stream exists for the narrow dtypes only
+    assert L.krex_gen_packed(None, k.F32, 4, 0, 0, 0, -1.0, 1.0, None) == k.EINVAL
+    assert L.krex_gen_packed(None, k.U32, 4, 0, 0, 0, -1.0, 1.0, None) == k.EINVAL
+    assert L.krex_gen_packed(ctypes.c_void_p(1), k.F16, 4, 0, 0, 0, -1.0, 1.0, None) == k.EALIGN
+    assert L.krex_gen_packed(None, k.F8E4M3, 4, 0, 0, 1, 0.0, -1.0, None) == k.EINVAL
+    assert L.krex_gen_packed(None, k.BF16, 0, 0, 0, 0, -1.0, 1.0, None) == k.OK
     assert L.krex_check(None, k.F32, None, k.F32, 4, -1.0, 0.0, ctypes.c_void_p(8), None) == k.EINVAL
     assert L.krex_check(None, k.F32, None, k.F32, 2**33, 0.0, 0.0, ctypes.c_void_p(8), None) == k.EINVAL
     assert L.krex_inject(None, None, k.F16, 4, 0, 0, 1.5, 0.5, 1, None) == k.EINVAL
