@@ -60,6 +60,7 @@ typedef int32_t krex_status;
 #define KREX_ENOMEM (-7)        /* host allocation failed */
 #define KREX_EPEER (-8)         /* shared segment unusable (version, peer died in init) */
 #define KREX_ESYS (-9)          /* POSIX call failed (shm, futex, threads) */
+#define KREX_EREVOKED (-10)     /* the region outlived its lease and was revoked */
 
 /* Element types. KREX_F8E4M3 is OCP fp8 e4m3fn (bias 7, max 448, no
  * infinity), gfx950's native fp8. KREX_U32 is the raw 32-bit word stream. */
@@ -212,7 +213,14 @@ krex_status krex_region_begin(void *stream, uint32_t timeout_ms, void *flush_buf
 
 /* Ends the region: waits for this process's region work to finish on the
  * device, reopens the gate, wakes parked siblings and releases the lock
- * (Section 4.2, step 8). KREX_ESTATE when not inside a region. */
+ * (Section 4.2, step 8). KREX_ESTATE when not inside a region.
+ * KREX_EREVOKED when the region outlived the segment's lease
+ * (KREX_REGION_LEASE_MS in the environment of the process that created the
+ * segment; unset or 0: no lease) and a parked sibling reopened the gate
+ * (Section 4.3: a client over its time limit is recovered like a dead one);
+ * the region is still left and the lock released, but timings taken in it
+ * were not exclusive. Revocation needs a running parked submitter, so it
+ * does not happen while CPU exclusivity has every sibling stopped. */
 krex_status krex_region_end(void *stream);
 
 /* --- timed loop ---------------------------------------------------------------
@@ -260,10 +268,23 @@ typedef struct krex_gate_stats {
     uint64_t park_ns;          /* time spent waiting there */
     uint64_t recoveries;       /* dead holders recovered by this process */
     uint64_t last_frozen;      /* processes stopped at the last entry (CPU exclusivity) */
+    uint64_t revocations;      /* regions of other processes revoked by this one (lease) */
     int32_t slot;              /* this process's registration slot, -1 if none */
     int32_t gated;             /* 1 if submissions are gated */
 } krex_gate_stats;
 krex_status krex_get_gate_stats(krex_gate_stats *out /* host */);
+
+/* --- health -----------------------------------------------------------------
+ * Context health check after a command (Section 4.3, context cleanup): waits
+ * for all of this process's work on its current device and reports whether
+ * the context is still usable. An unhealthy context (a sticky device error,
+ * or `stream` left in graph capture) marks this process's slot failed:
+ * region entries stop waiting for its work and its further submissions are
+ * refused with KREX_EHIP, so the caller must retire the process. Returns
+ * KREX_OK, KREX_EHIP (device error; see krex_last_hip_error) or KREX_ESTATE
+ * (capture in progress). The completion tracker marks the slot failed the
+ * same way when waiting for a counted operation reports an error. */
+krex_status krex_health_check(void *stream);
 
 const char *krex_strerror(krex_status st);
 int32_t krex_last_hip_error(void);

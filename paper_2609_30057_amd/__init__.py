@@ -32,7 +32,8 @@ ATTACH_CPU_EXCLUSIVE = 2
 PROBE_THREADS = 65536
 
 OK, RECOVERED = 0, 1
-EINVAL, EALIGN, EHIP, ETIMEDOUT, ESTATE, ENOTATTACHED, ENOMEM, EPEER, ESYS = -1, -2, -3, -4, -5, -6, -7, -8, -9
+EINVAL, EALIGN, EHIP, ETIMEDOUT, ESTATE, ENOTATTACHED, ENOMEM, EPEER, ESYS, EREVOKED = (
+    -1, -2, -3, -4, -5, -6, -7, -8, -9, -10)
 
 _DISTS = {"uniform": UNIFORM, "normal": NORMAL, "bitcast": BITCAST}
 _MODES = {"round": INJ_ROUND, "exact": INJ_EXACT}
@@ -67,7 +68,7 @@ class _SgemmArgs(ctypes.Structure):
 class _GateStats(ctypes.Structure):
     _fields_ = [("regions", ctypes.c_uint64), ("last_drain_ns", ctypes.c_uint64),
                 ("total_drain_ns", ctypes.c_uint64), ("parks", ctypes.c_uint64), ("park_ns", ctypes.c_uint64),
-                ("recoveries", ctypes.c_uint64), ("last_frozen", ctypes.c_uint64),
+                ("recoveries", ctypes.c_uint64), ("last_frozen", ctypes.c_uint64), ("revocations", ctypes.c_uint64),
                 ("slot", ctypes.c_int32), ("gated", ctypes.c_int32)]
 
 
@@ -117,6 +118,7 @@ def lib():
             "krex_time_loop": (i32, [LAUNCH_FN, vp, u32, u32, vp, u64, u32, u32, vp, vp, vp]),
             "krex_fixture_sgemm": (i32, [u32, u32, u32, vp, vp, vp, vp]),
             "krex_get_gate_stats": (i32, [vp]),
+            "krex_health_check": (i32, [vp]),
             "krex_strerror": (ctypes.c_char_p, [i32]),
             "krex_last_hip_error": (i32, []),
             "krex_version": (ctypes.c_char_p, []),
@@ -313,6 +315,12 @@ class region:
             yield
         finally:
             region_end(stream)
+
+
+def health_check(stream=None):
+    """Context health after a command (Section 4.3): raises KrexError and marks
+    this process's slot failed if the context is no longer usable."""
+    return _chk(lib().krex_health_check(_stream(stream)), "krex_health_check")
 
 
 def gate_stats():

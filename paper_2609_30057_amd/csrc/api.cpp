@@ -148,7 +148,9 @@ private:
                 hipSetDevice(it.dev);
                 cur = it.dev;
             }
-            hipEventSynchronize(it.ev);
+            // A failed wait means the context hit a device error: the count is
+            // released and the slot marked failed (no sibling waits on it).
+            if (hipEventSynchronize(it.ev) != hipSuccess) krexg::mark_failed();
             krexg::release(1);
             give_event(it.dev, it.ev);
             pending_.fetch_sub(1);
@@ -539,9 +541,26 @@ krex_status krex_get_gate_stats(krex_gate_stats *out)
     out->park_ns = st.park_ns;
     out->recoveries = st.recoveries;
     out->last_frozen = st.last_frozen;
+    out->revocations = st.revocations;
     out->slot = st.slot;
     out->gated = st.gated;
     return KREX_OK;
+}
+
+krex_status krex_health_check(void *stream)
+{
+    hipStream_t s = (hipStream_t)stream;
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &cs) == hipSuccess && cs != hipStreamCaptureStatusNone) {
+        krexg::mark_failed();
+        return KREX_ESTATE;
+    }
+    const hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) {
+        krexg::mark_failed();
+        return hip_fail(e);
+    }
+    return krexg::failed() ? KREX_EHIP : KREX_OK;
 }
 
 const char *krex_strerror(krex_status st)
@@ -558,6 +577,7 @@ const char *krex_strerror(krex_status st)
     case KREX_ENOMEM: return "out of host memory";
     case KREX_EPEER: return "shared segment unusable";
     case KREX_ESYS: return "system call failed";
+    case KREX_EREVOKED: return "region revoked after its lease expired";
     default: return "unknown status";
     }
 }

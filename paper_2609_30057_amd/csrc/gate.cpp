@@ -29,12 +29,12 @@ namespace krexg {
 namespace {
 
 constexpr uint64_t kMagic = 0x4b52455847415445ull;   // "KREXGATE"
-constexpr uint32_t kVersion = 4;
+constexpr uint32_t kVersion = 5;
 constexpr uint64_t kEpochMask = (1ull << 48) - 1;
 
 struct alignas(64) Slot {
     std::atomic<int32_t> pid;          // 0 = free
-    std::atomic<uint32_t> flags;       // kNoGate
+    std::atomic<uint32_t> flags;       // kNoGate, kCpuExclusive, kFailed
     std::atomic<uint64_t> start_time;  // /proc start time of pid, guards pid reuse
     std::atomic<int64_t> inflight;     // counted submissions not yet completed
     std::atomic<uint64_t> frozen_by;   // gate word of the region that stopped this process; 0 = running
@@ -49,6 +49,9 @@ struct Segment {
     alignas(64) std::atomic<uint32_t> gate_seq;  // futex word, bumped on every gate change
     std::atomic<uint32_t> parked;                // processes parked on gate_seq
     alignas(64) std::atomic<uint64_t> epoch;
+    std::atomic<uint64_t> gate_since;  // CLOCK_MONOTONIC ns when the current gate closed
+    std::atomic<uint64_t> lease_ns;    // region lease (0: none), fixed by the segment's creator
+    std::atomic<uint64_t> revoked;     // gate word of the last revoked region
     Slot slots[kSlots];
 };
 
@@ -68,6 +71,7 @@ struct State {
     cpu_set_t saved_affinity;
     std::atomic<uint64_t> regions{0}, last_drain_ns{0}, total_drain_ns{0}, parks{0}, park_ns{0}, recoveries{0};
     std::atomic<uint64_t> last_frozen{0};
+    std::atomic<uint64_t> revocations{0};
 };
 
 State &st()
@@ -248,6 +252,24 @@ void open_gate(Segment *seg, uint64_t epoch)
     futex_wake_all(&seg->gate_seq);
 }
 
+// Revokes the region whose gate word is g once it has outlived the lease
+// (Section 4.3: a client exceeding its time limit is recovered like a dead
+// one). Bound to the holder and epoch: the compare-and-swap succeeds only
+// while g is still the gate, so a late revocation never reopens a later
+// region. The holder keeps the region lock; its region exit reports the
+// revocation.
+bool revoke(Segment *seg, uint64_t g)
+{
+    uint64_t expect = g;
+    if (!seg->gate.compare_exchange_strong(expect, g & kEpochMask, std::memory_order_seq_cst)) return false;
+    thaw_region(seg, g);
+    seg->revoked.store(g, std::memory_order_seq_cst);
+    seg->gate_seq.fetch_add(1, std::memory_order_seq_cst);
+    futex_wake_all(&seg->gate_seq);
+    st().revocations.fetch_add(1);
+    return true;
+}
+
 // Called with the region lock held after EOWNERDEAD: the previous holder died
 // inside its region. Reopen its gate (only if it is still that holder's
 // closure) and free its slot.
@@ -344,6 +366,8 @@ int map_segment(const char *name, Segment **out)
         pthread_mutexattr_destroy(&a);
         seg->version = kVersion;
         seg->nslots = kSlots;
+        if (const char *e = getenv("KREX_REGION_LEASE_MS"))
+            seg->lease_ns.store((uint64_t)strtoull(e, nullptr, 10) * 1000000ull);
         seg->magic.store(kMagic, std::memory_order_release);
     } else {
         const uint64_t deadline = now_ns() + 5000000000ull;
@@ -474,6 +498,7 @@ int admit(uint64_t timeout_ns, bool *counted)
     Segment *seg = s.seg;
     if (!seg || !s.gated_) return KREX_OK;
     Slot &me = seg->slots[s.slot];
+    if (me.flags.load() & kFailed) return KREX_EHIP;   // failed health: no further submissions
     const uint32_t mine = (uint32_t)s.slot + 1;
     uint64_t t_park = 0;
     const uint64_t start = now_ns();
@@ -518,9 +543,29 @@ int admit(uint64_t timeout_ns, bool *counted)
         seg->parked.fetch_sub(1, std::memory_order_seq_cst);
         if (seg->gate.load(std::memory_order_seq_cst) == g) {
             Slot &hs = seg->slots[h - 1];
-            if (!alive(hs.pid.load(), hs.start_time.load())) try_recover(seg);
+            if (!alive(hs.pid.load(), hs.start_time.load())) {
+                try_recover(seg);
+            } else {
+                const uint64_t lease = seg->lease_ns.load();
+                if (lease && now_ns() - seg->gate_since.load() > lease) revoke(seg, g);
+            }
         }
     }
+}
+
+void mark_failed()
+{
+    State &s = st();
+    if (!s.seg || s.slot < 0) return;
+    Slot &me = s.seg->slots[s.slot];
+    me.flags.fetch_or(kFailed);
+    me.inflight.store(0);          // a failed context's counts are not waited for
+}
+
+bool failed()
+{
+    State &s = st();
+    return s.seg && s.slot >= 0 && (s.seg->slots[s.slot].flags.load() & kFailed);
 }
 
 void release(uint64_t k)
@@ -563,6 +608,7 @@ int region_begin(uint32_t timeout_ms)
     }
     // Step 2: close the gate with this process as holder and a new epoch.
     const uint64_t epoch = seg->epoch.fetch_add(1, std::memory_order_seq_cst) + 1;
+    seg->gate_since.store(now_ns(), std::memory_order_seq_cst);
     seg->gate.store(((uint64_t)(s.slot + 1) << 48) | (epoch & kEpochMask), std::memory_order_seq_cst);
     seg->gate_seq.fetch_add(1, std::memory_order_seq_cst);
     // Step 3: wait until every other gated process has nothing in flight.
@@ -574,7 +620,7 @@ int region_begin(uint32_t timeout_ms)
         uint64_t next_liveness = now_ns() + 10000000ull;
         for (;;) {
             const int32_t pid = sl.pid.load(std::memory_order_seq_cst);
-            if (pid == 0 || (sl.flags.load() & kNoGate)) break;
+            if (pid == 0 || (sl.flags.load() & (kNoGate | kFailed))) break;
             if (sl.inflight.load(std::memory_order_seq_cst) <= 0) break;
             const uint64_t now = now_ns();
             if (now >= next_liveness) {
@@ -653,16 +699,22 @@ int region_end()
     if (!seg) return KREX_ENOTATTACHED;
     if (!s.in_region) return KREX_ESTATE;
     // Step 7: resume stopped siblings and unpin; step 8: reopen the gate,
-    // wake parked siblings, release the lock.
+    // wake parked siblings, release the lock. The reopening is a
+    // compare-and-swap from this region's gate word, so exactly one of this
+    // exit and a lease revocation reopens it; if the revocation won, the
+    // region is reported as revoked (its timings are not exclusive).
     if (s.flags & kCpuExclusive) thaw_region(seg, s.region_gate);
     if (s.pinned) {
         sched_setaffinity(0, sizeof(cpu_set_t), &s.saved_affinity);
         s.pinned = false;
     }
-    open_gate(seg, seg->gate.load() & kEpochMask);
+    uint64_t expect = s.region_gate;
+    const bool ours = seg->gate.compare_exchange_strong(expect, s.region_gate & kEpochMask, std::memory_order_seq_cst);
+    seg->gate_seq.fetch_add(1, std::memory_order_seq_cst);
+    futex_wake_all(&seg->gate_seq);
     s.in_region = false;
     pthread_mutex_unlock(&seg->lock);
-    return KREX_OK;
+    return ours ? KREX_OK : KREX_EREVOKED;
 }
 
 void get_stats(Stats *out)
@@ -675,6 +727,7 @@ void get_stats(Stats *out)
     out->park_ns = s.park_ns.load();
     out->recoveries = s.recoveries.load();
     out->last_frozen = s.last_frozen.load();
+    out->revocations = s.revocations.load();
     out->slot = s.slot;
     out->gated = s.seg && s.gated_ ? 1 : 0;
 }

@@ -17,7 +17,11 @@
 // processes after the drain and pins its own thread (Section 4.2, steps 4
 // and 5), and resumes them before the gate reopens (step 7); the stop is
 // SIGSTOP / SIGCONT of the registered processes, recorded in shared memory
-// so that recovery from the holder's death resumes them.
+// so that recovery from the holder's death resumes them. A region that
+// outlives the segment's lease (KREX_REGION_LEASE_MS of the process that
+// created the segment; 0 or unset: no lease) is revoked by a parked
+// submitter: the gate reopens (bound to the region's holder and epoch) and
+// the holder's exit returns KREX_EREVOKED (Section 4.3, time limits).
 //
 // This file is plain POSIX C++ (no HIP): the GPU-side completion tracking
 // lives in the ABI layer, and the CPU tests drive the same code with a fake
@@ -36,12 +40,14 @@ struct Stats {
     uint64_t park_ns;
     uint64_t recoveries;
     uint64_t last_frozen;
+    uint64_t revocations;
     int32_t slot;
     int32_t gated;
 };
 
 constexpr uint32_t kNoGate = 1u;          // register, never block or count
 constexpr uint32_t kCpuExclusive = 2u;    // as holder: stop siblings, pin the region thread
+constexpr uint32_t kFailed = 4u;          // slot state: failed health check, never waited for
 constexpr int kSlots = 64;
 
 // All functions return krex status codes (KREX_OK, KREX_E*).
@@ -59,6 +65,11 @@ bool in_region();
 int admit(uint64_t timeout_ns, bool *counted);
 // Releases k counted submissions (device completion or launch failure).
 void release(uint64_t k);
+// Marks this process's slot failed (a sticky device error or an unusable
+// context, Section 4.3): entries stop waiting for its work and its further
+// submissions are refused with KREX_EHIP.
+void mark_failed();
+bool failed();
 int64_t inflight_self();
 
 // Region entry after the caller's own work has finished (steps 1-3); exit

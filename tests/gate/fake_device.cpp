@@ -141,6 +141,9 @@ int kg_region_end()
 
 int64_t kg_inflight() { return krexg::inflight_self(); }
 
+// What the library does when a context fails its health check.
+void kg_fail() { krexg::mark_failed(); }
+
 uint64_t kg_now() { return now_ns(); }
 
 void kg_stats(krexg::Stats *out) { krexg::get_stats(out); }

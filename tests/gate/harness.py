@@ -32,7 +32,7 @@ def build(variant=""):
 class Stats(ctypes.Structure):
     _fields_ = [("regions", ctypes.c_uint64), ("last_drain_ns", ctypes.c_uint64),
                 ("total_drain_ns", ctypes.c_uint64), ("parks", ctypes.c_uint64), ("park_ns", ctypes.c_uint64),
-                ("recoveries", ctypes.c_uint64), ("last_frozen", ctypes.c_uint64),
+                ("recoveries", ctypes.c_uint64), ("last_frozen", ctypes.c_uint64), ("revocations", ctypes.c_uint64),
                 ("slot", ctypes.c_int32), ("gated", ctypes.c_int32)]
 
 
@@ -46,6 +46,7 @@ def load(variant=""):
     L.kg_now.restype = ctypes.c_uint64
     L.kg_stats.argtypes = [ctypes.POINTER(Stats)]
     L.kg_log_get.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_uint64)]
+    L.kg_fail.restype = None
     return L
 
 

@@ -162,3 +162,61 @@ def registered_parent_of_holder(name, counter, q):
     child.join(60)
     q.put(("parent", child.exitcode, got))
     L.kg_detach()
+
+
+def long_op_then_fail(name, dur_us, ready):
+    """Submits one long operation, then fails its health check (its work
+    would still be in flight) and stays alive."""
+    L = _L()
+    assert L.kg_attach(name.encode(), 0) == OK
+    assert L.kg_submit(dur_us, 0, None) == OK
+    L.kg_fail()
+    ready.set()
+    time.sleep(600)
+
+
+def fail_then_submit(name, q):
+    L = _L()
+    assert L.kg_attach(name.encode(), 0) == OK
+    assert L.kg_submit(100, 0, None) == OK
+    L.kg_wait_idle(10000)
+    L.kg_fail()
+    rc = L.kg_submit(100, 0, None)
+    q.put(("failed_submit", rc))
+    L.kg_detach()
+
+
+def hold_past_lease(name, hold_s, second_ms, ready, ready2, q):
+    """Holds a region for hold_s (beyond the lease), then a short second one
+    (within it), signalling ready2 once inside the second."""
+    L = _L()
+    assert L.kg_attach(name.encode(), 0) == OK
+    assert L.kg_region_begin(10000) == OK
+    t_in = L.kg_now()
+    ready.set()
+    time.sleep(hold_s)
+    rc1 = L.kg_region_end()
+    assert L.kg_region_begin(10000) == OK
+    t2_in = L.kg_now()
+    ready2.set()
+    time.sleep(second_ms / 1000)
+    t2_out = L.kg_now()
+    rc2 = L.kg_region_end()
+    q.put(("holder", rc1, rc2, t_in, t2_in, t2_out))
+    L.kg_detach()
+
+
+def submit_twice(name, ready2, q):
+    """Two submissions: the first parks until the first region is revoked,
+    the second is made inside the holder's short second region."""
+    L = _L()
+    assert L.kg_attach(name.encode(), 0) == OK
+    t = ctypes.c_uint64()
+    rc = L.kg_submit(100, 10**10, ctypes.byref(t))
+    t1 = t.value
+    assert ready2.wait(30)
+    rc2 = L.kg_submit(100, 10**10, ctypes.byref(t))
+    t2 = t.value
+    L.kg_wait_idle(10000)
+    q.put(("sib", rc, t1, rc2, t2, harness.stats(L)))
+    L.kg_detach()

@@ -47,7 +47,8 @@ def test_constants_match_binding():
              "KREX_U32": k.U32, "KREX_UNIFORM": k.UNIFORM, "KREX_NORMAL": k.NORMAL, "KREX_BITCAST": k.BITCAST,
              "KREX_INJ_ROUND": k.INJ_ROUND, "KREX_INJ_EXACT": k.INJ_EXACT, "KREX_TL_REGION": k.TL_REGION,
              "KREX_ATTACH_NO_GATE": k.ATTACH_NO_GATE,
-             "KREX_ATTACH_CPU_EXCLUSIVE": k.ATTACH_CPU_EXCLUSIVE, "KREX_PROBE_THREADS": k.PROBE_THREADS,
+             "KREX_ATTACH_CPU_EXCLUSIVE": k.ATTACH_CPU_EXCLUSIVE,
+             "KREX_EREVOKED": k.EREVOKED, "KREX_PROBE_THREADS": k.PROBE_THREADS,
              "KREX_OK": k.OK, "KREX_RECOVERED": k.RECOVERED, "KREX_EINVAL": k.EINVAL, "KREX_EALIGN": k.EALIGN,
              "KREX_EHIP": k.EHIP, "KREX_ETIMEDOUT": k.ETIMEDOUT, "KREX_ESTATE": k.ESTATE,
              "KREX_ENOTATTACHED": k.ENOTATTACHED, "KREX_ENOMEM": k.ENOMEM, "KREX_EPEER": k.EPEER,

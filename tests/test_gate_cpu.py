@@ -323,3 +323,58 @@ def test_cpu_exclusive_holder_below_registered_parent(shm_name):
     assert tag == "parent" and exitcode == 0
     assert got[0] == "excl" and len(got[2]) == 2
     assert all(r[5] >= 1 for r in got[2])       # the parent (at least) was stopped
+
+
+def test_failed_sibling_is_not_waited_for(shm_name):
+    """Section 4.3: a context that failed its health check is retired; region
+    entry does not wait for the work it still had in flight."""
+    ready = CTX.Event()
+    sib = CTX.Process(target=workers.long_op_then_fail, args=(shm_name, 3_000_000, ready))
+    sib.start()
+    try:
+        assert ready.wait(30)
+        q = CTX.Queue()
+        b = CTX.Process(target=workers.try_region, args=(shm_name, 10000, q))
+        b.start()
+        tag, rc, dt, _ = q.get(timeout=60)
+        b.join(30)
+        assert tag == "try" and rc == OK and dt < 1.0, (rc, dt)
+    finally:
+        sib.kill()
+        sib.join(30)
+
+
+def test_failed_process_cannot_submit(shm_name):
+    q = CTX.Queue()
+    p = CTX.Process(target=workers.fail_then_submit, args=(shm_name, q))
+    p.start()
+    tag, rc = q.get(timeout=60)
+    _join([p])
+    assert tag == "failed_submit" and rc == -3       # KREX_EHIP
+
+
+def test_region_revoked_after_its_lease(shm_name, monkeypatch):
+    """Section 4.3 (time limits): with a 300 ms lease, a parked submitter
+    reopens a region held for 1.5 s; the holder's exit reports the
+    revocation; the holder's next, short region is not revoked (the
+    revocation is bound to the region's gate word) and the sibling's next
+    submission waits for it as usual."""
+    monkeypatch.setenv("KREX_REGION_LEASE_MS", "300")
+    q = CTX.Queue()
+    ready, ready2 = CTX.Event(), CTX.Event()
+    holder = CTX.Process(target=workers.hold_past_lease, args=(shm_name, 1.5, 200, ready, ready2, q))
+    holder.start()
+    assert ready.wait(30)
+    sib = CTX.Process(target=workers.submit_twice, args=(shm_name, ready2, q))
+    sib.start()
+    res = _collect(q, 2)
+    _join([holder, sib])
+    h = [r for r in res if r[0] == "holder"][0]
+    s = [r for r in res if r[0] == "sib"][0]
+    _, rc1, rc2, t_in, t2_in, t2_out = h
+    _, srw, t1, srw2, t2, st = s
+    assert rc1 == -10 and rc2 == OK                 # KREX_EREVOKED, then a normal exit
+    assert srw == OK and srw2 == OK
+    assert 0.25e9 < t1 - t_in < 1.2e9               # admitted once the lease ran out
+    assert st["revocations"] == 1
+    assert t2 >= t2_out                             # the second region kept its exclusivity

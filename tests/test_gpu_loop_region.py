@@ -199,3 +199,39 @@ def test_two_processes_share_gpu_invariant_results(shm_name, cpu_exclusive):
     assert rounds > 3 and results == [solo_key]
     assert drains["regions"] == 10
     assert frozen == ([1] * 10 if cpu_exclusive else [0] * 10)
+
+
+def test_health_check(shm_name):
+    """Section 4.3: a healthy context passes; a stream left in graph capture
+    fails the check, which retires the process's slot (further submissions
+    are refused)."""
+    krex.attach(shm_name=shm_name)
+    try:
+        x = empty("f16", 1 << 20)
+        krex.gen(x, 1)
+        assert krex.health_check() == krex.OK
+        s = torch.cuda.Stream()
+        g = torch.cuda.CUDAGraph()
+        y = torch.zeros(16, device="cuda")
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s):
+            g.capture_begin()
+            try:
+                y.add_(1.0)
+                with pytest.raises(krex.KrexError) as e:
+                    krex.health_check(stream=s)
+                assert e.value.status == krex.ESTATE
+            finally:
+                g.capture_end()
+        torch.cuda.synchronize()
+        with pytest.raises(krex.KrexError) as e:
+            krex.gen(x, 1)
+        assert e.value.status == krex.EHIP
+    finally:
+        krex.detach()
+    krex.attach(shm_name=shm_name)                # a new registration starts healthy
+    try:
+        krex.gen(x, 1)
+        assert krex.health_check() == krex.OK
+    finally:
+        krex.detach()
