@@ -1,7 +1,14 @@
-"""Builds libkrex.so (the C ABI of include/krex.h) for gfx950 with hipcc.
+"""Builds the three shared libraries of the package with hipcc:
 
-kernels.hip is compiled as HIP for --offload-arch=gfx950; api.cpp and gate.cpp
-are host C++ against the HIP runtime. Floating-point flags fix the semantics
+  libkrexgate.so       the region coordinator (gate.cpp, plain POSIX C++),
+                       one instance per process for both libraries below;
+  libkrex.so           the C ABI of include/krex.h: kernels.hip for gfx950 and
+                       api.cpp (host C++ against the HIP runtime);
+  libkrex_intercept.so the ROCm tools library of include/krex_intercept.h
+                       (loaded through HSA_TOOLS_LIB).
+
+kernels.hip is compiled as HIP for --offload-arch=gfx950; the rest is host
+C++. Floating-point flags fix the semantics
 the generated values and check verdicts are defined with: no contraction
 into fused multiply-adds except where written, correctly rounded fp32
 division and square root, fp32 denormals kept. Packed fp32 instructions are
@@ -17,6 +24,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libkrex.so")
+GATE_LIB = os.path.join(HERE, "libkrexgate.so")
+INTERCEPT_LIB = os.path.join(HERE, "libkrex_intercept.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
@@ -27,7 +36,10 @@ DEVICE = ["-x", "hip", "--offload-arch=" + ARCH, "-ffp-contract=off",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 HOST = ["-x", "c++", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include"]
 
-SOURCES = [("kernels.hip", DEVICE), ("api.cpp", HOST), ("gate.cpp", HOST)]
+# The HSA tools header includes its siblings by bare name under this macro.
+INTERCEPT = HOST + ["-DAMD_INTERNAL_BUILD", "-I/opt/rocm/include/hsa"]
+
+SOURCES = [("kernels.hip", DEVICE), ("api.cpp", HOST), ("gate.cpp", HOST), ("intercept.cpp", INTERCEPT)]
 
 
 def _compile(src, flags, verbose):
@@ -41,18 +53,27 @@ def _compile(src, flags, verbose):
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
-    with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(lambda sf: _compile(sf[0], sf[1], verbose), SOURCES))
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [HIPCC, "-shared", "-fPIC", "--offload-arch=" + ARCH, *objs, "-o", tmp, "-lpthread", "-lrt"]
+def _link(out, objs, extra, verbose, linker=HIPCC):
+    tmp = out + ".tmp%d" % os.getpid()
+    cmd = [linker, "-shared", "-fPIC", *objs, "-o", tmp, *extra]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed: %s\n%s%s" % (" ".join(cmd), r.stdout, r.stderr))
-    os.replace(tmp, LIB)
+    os.replace(tmp, out)
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
+        kernels, api, gate, intercept = ex.map(lambda sf: _compile(sf[0], sf[1], verbose), SOURCES)
+    rpath = ["-L" + HERE, "-lkrexgate", "-Wl,-rpath,$ORIGIN", "-lpthread", "-lrt"]
+    # The coordinator and the interceptor are plain host code: linked without
+    # the HIP runtime (the interceptor loads inside the HSA runtime's start).
+    _link(GATE_LIB, [gate], ["-Wl,-soname,libkrexgate.so", "-lpthread", "-lrt"], verbose, linker="g++")
+    _link(LIB, [kernels, api], ["--offload-arch=" + ARCH, *rpath], verbose)
+    _link(INTERCEPT_LIB, [intercept], rpath, verbose, linker="g++")
     return LIB
 
 

@@ -192,6 +192,13 @@ uint64_t gate_timeout_ns()
 template <typename F>
 krex_status submit(hipStream_t s, F &&launch_fn)
 {
+    // With the dispatch interceptor active every kernel is counted at its
+    // queue; counting here too could hold a count while the same launch
+    // waits at the gate.
+    if (krexg::intercepted()) {
+        const hipError_t e = launch_fn();
+        return e == hipSuccess ? KREX_OK : hip_fail(e);
+    }
     bool counted = false;
     const int rc = krexg::admit(gate_timeout_ns(), &counted);
     if (rc != KREX_OK) return rc;
@@ -280,6 +287,13 @@ extern "C" {
 krex_status krex_attach(int32_t device, const char *shm_name, uint32_t flags)
 {
     if (flags & ~(KREX_ATTACH_NO_GATE | KREX_ATTACH_CPU_EXCLUSIVE)) return KREX_EINVAL;
+    if (krexg::intercepted() && krexg::attached()) {
+        // Registered by the dispatch interceptor: reuse that registration.
+        if (((flags & KREX_ATTACH_NO_GATE) != 0) != ((krexg::flags() & krexg::kNoGate) != 0)) return KREX_ESTATE;
+        krexg::set_cpu_exclusive((flags & KREX_ATTACH_CPU_EXCLUSIVE) != 0);
+        g_device_attached = device;
+        return KREX_OK;
+    }
     char name[256];
     if (shm_name) {
         if (strlen(shm_name) >= sizeof name) return KREX_EINVAL;
@@ -303,6 +317,7 @@ krex_status krex_detach(void)
 {
     if (!krexg::attached()) return KREX_ESTATE;
     if (krexg::in_region()) return KREX_ESTATE;
+    if (krexg::intercepted()) return KREX_OK;   // the interceptor's registration stays
     if (!Tracker::instance().drain(60000)) return KREX_ETIMEDOUT;
     const int rc = krexg::detach();
     if (rc == KREX_OK) g_device_attached = -1;
@@ -490,7 +505,7 @@ krex_status krex_time_loop(krex_launch_fn fn, void *user, uint32_t warmup, uint3
     if (region) {
         entry = krex_region_begin(stream, timeout_ms, nullptr, 0);
         if (entry < 0) return entry;   // a failed entry starts no measurement
-    } else {
+    } else if (!krexg::intercepted()) {
         rc = krexg::admit(gate_timeout_ns(), &counted);
         if (rc != KREX_OK) return rc;
     }

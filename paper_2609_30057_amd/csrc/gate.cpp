@@ -562,6 +562,24 @@ void mark_failed()
     me.inflight.store(0);          // a failed context's counts are not waited for
 }
 
+std::atomic<bool> g_intercepted{false};
+
+void set_intercepted(bool on) { g_intercepted.store(on); }
+bool intercepted() { return g_intercepted.load(); }
+
+void set_cpu_exclusive(bool on)
+{
+    State &s = st();
+    std::lock_guard<std::mutex> g(s.mu);
+    s.flags = on ? (s.flags | kCpuExclusive) : (s.flags & ~kCpuExclusive);
+    if (s.seg && s.slot >= 0) {
+        if (on) s.seg->slots[s.slot].flags.fetch_or(kCpuExclusive);
+        else s.seg->slots[s.slot].flags.fetch_and(~kCpuExclusive);
+    }
+}
+
+uint32_t flags() { return st().flags; }
+
 bool failed()
 {
     State &s = st();

@@ -70,6 +70,14 @@ void release(uint64_t k);
 // submissions are refused with KREX_EHIP.
 void mark_failed();
 bool failed();
+// Set by the dispatch interceptor once it registered this process: every
+// kernel dispatch is then counted at the queue, so callers stop counting
+// their own launches.
+void set_intercepted(bool on);
+bool intercepted();
+// Updates the CPU-exclusivity choice of an existing registration.
+void set_cpu_exclusive(bool on);
+uint32_t flags();
 int64_t inflight_self();
 
 // Region entry after the caller's own work has finished (steps 1-3); exit

@@ -31,6 +31,23 @@ def test_header_declares_the_boundary():
         assert n in names
 
 
+def test_interceptor_exports_its_header():
+    from paper_2609_30057_amd.build import INTERCEPT_LIB
+    if not os.path.exists(INTERCEPT_LIB):
+        pytest.fail("libkrex_intercept.so is not built; run __graft_entry__.build()")
+    text = open(os.path.join(ROOT, "include", "krex_intercept.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = set(re.findall(r"^\s*[a-z_0-9]+\s*\*?\s*(krex_[a-z_0-9]+)\s*\(", text, flags=re.M))
+    assert names == {"krex_intercept_stats", "krex_intercept_log"}
+    L = ctypes.CDLL(INTERCEPT_LIB)
+    for n in sorted(names) + ["OnLoad", "OnUnload"]:
+        assert hasattr(L, n), n
+    # loaded outside the HSA runtime it is inactive and reports so
+    buf = (ctypes.c_uint64 * 6)()
+    assert L.krex_intercept_stats(buf) == 0 and buf[5] == 0
+    assert L.krex_intercept_log(None, None, 10) == 0
+
+
 def test_library_exports_every_declared_function():
     from paper_2609_30057_amd import LIB_PATH
     if not os.path.exists(LIB_PATH):
