@@ -17,7 +17,8 @@ the step's 200.2 GiB). The timed-region inflation half of the metric is
 measured by `--fidelity` (Section 6.3, Eq. 1), which prints its own line.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
-       python bench.py --fidelity [--samples S] [--siblings N] [--modes control,gated,ungated,frozen]
+       python bench.py --fidelity [--samples S] [--siblings N] [--warmup-ms W]
+                              [--modes control,gated,ungated,frozen,frozen_nopin,torch_gated,torch_ungated]
        python bench.py --kernels          per-kernel throughput on the command shapes
        python bench.py --configs          the other commands: gemm_tiny, check_stress, mixed_stream
        python bench.py --calib-copy       also time a plain 1 GiB device copy (the
@@ -402,6 +403,8 @@ def main():
     ap.add_argument("--fidelity", action="store_true")
     ap.add_argument("--samples", type=int, default=None)
     ap.add_argument("--siblings", type=int, default=None, help="fidelity sibling processes (default 7)")
+    ap.add_argument("--warmup-ms", type=float, default=None,
+                    help="fidelity: in-region warm-up time per sample (default 3 ms; 0: one warm-up launch)")
     ap.add_argument("--modes", default=None,
                     help="fidelity modes, comma-separated from control,gated,ungated,frozen")
     ap.add_argument("--kernels", action="store_true")
@@ -414,7 +417,8 @@ def main():
     if args.fidelity:
         from paper_2609_30057_amd import fidelity
         modes = args.modes.split(",") if args.modes else None
-        print(json.dumps(fidelity.run(samples=args.samples, modes=modes, siblings=args.siblings)), flush=True)
+        print(json.dumps(fidelity.run(samples=args.samples, modes=modes, siblings=args.siblings,
+                                      warmup_ms=args.warmup_ms)), flush=True)
         return
     if args.kernels:
         print(json.dumps(run_kernels()), flush=True)
