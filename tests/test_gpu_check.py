@@ -4,6 +4,7 @@ patterns), near-equal inputs with injected mismatches, all 16 dtype pairs,
 ragged and tiny sizes, misaligned operands, and repeated calls reusing one
 result buffer."""
 import numpy as np
+import torch
 import pytest
 
 import oracle
@@ -147,3 +148,37 @@ def test_max_rel_search_matches_oracle(kind):
             ref = oracle.check(ac, dta, bc, dtb, 1e-3, 1e-5)
             r = krex.check(from_storage(ac, dta), from_storage(bc, dtb), 1e-3, 1e-5)
             same_result(r, ref)
+
+
+def test_check_at_the_maximum_size():
+    """n = 2^33 - 1 (the largest n the boundary accepts), fp8 operands of
+    8 GiB each: three planted differences, two beyond index 2^32; the record
+    follows in closed form (mismatch count, the largest difference and its
+    index, max_rel)."""
+    n = 2**33 - 1
+    a = torch.zeros(n, dtype=torch.float8_e4m3fn, device="cuda")
+    b = torch.zeros(n, dtype=torch.float8_e4m3fn, device="cuda")
+    b8 = b.view(torch.uint8)
+    a8 = a.view(torch.uint8)
+    # b = 1.0 (0x38) at the planted indices; a = 1.5 (0x3C), 3.0 (0x44), 1.125 (0x39)
+    idx = [3, 2**32 + 5, n - 1]
+    for i, av in zip(idx, (0x3C, 0x44, 0x39)):
+        b8[i] = 0x38
+        a8[i] = av
+    r = krex.check(a, b, 0.0, 0.0)
+    assert (r.n, r.mismatches, r.nan_count) == (n, 3, 0)
+    assert r.argmax_abs == 2**32 + 5 and r.max_abs == 2.0 and r.max_rel == 2.0
+    del a, b
+
+
+def test_check_beyond_the_maximum_size_is_rejected():
+    x = torch.empty(16, dtype=torch.float32, device="cuda")
+    out = krex.check_result_buffer()
+    L = krex.lib()
+    assert L.krex_check(ctypes_ptr(x), krex.F32, ctypes_ptr(x), krex.F32, 2**33, 0.0, 0.0, ctypes_ptr(out),
+                        None) == krex.EINVAL
+
+
+def ctypes_ptr(t):
+    import ctypes
+    return ctypes.c_void_p(t.data_ptr())

@@ -128,3 +128,17 @@ def test_gen_rejects_bad_arguments():
         krex.gen(t, 0, 2**64 - 3)
     with pytest.raises(krex.KrexError):
         krex.gen(t, 0, 0, "normal", 0.0, -1.0)
+
+
+def test_gen_beyond_2_to_32_elements():
+    """4 GiB of fp8 in one launch (n > 2^32) at an offset near the top of the
+    word stream: elements on both sides of index 2^32 match the oracle."""
+    n = 2**32 + 7
+    off = 2**64 - n - 3
+    t = empty("f8", n)
+    krex.gen(t, 11, off, 0, -1.0, 1.0)
+    idx = np.array([0, 1, 2**31, 2**32 - 1, 2**32, 2**32 + 1, n - 1])
+    got = to_storage(t[torch.from_numpy(idx).cuda()], "f8")
+    ref = np.concatenate([oracle.gen("f8", 1, 11, off + int(i), 0, -1.0, 1.0) for i in idx])
+    assert_bits_equal(got, ref, "f8 > 2^32")
+    del t
