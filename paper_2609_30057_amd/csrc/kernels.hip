@@ -77,20 +77,18 @@ __global__ __launch_bounds__(kThreads) void k_gen(GenParams P)
         const uint64_t bfirst = P.b0 + g * G;
         union {
             uint4 v;
+            uint32_t w[4];
             T s[4 * G];
         } pk;
+        if constexpr (DT == U32) {
+            const words4 w = philox_block(bfirst, P.k0, P.k1);
 #pragma unroll
-        for (int i = 0; i < G; ++i) {
-            const words4 w = philox_block(bfirst + i, P.k0, P.k1);
-            if constexpr (DT == U32) {
+            for (int l = 0; l < 4; ++l) pk.w[l] = w.v[l];
+        } else {
+            float v[4 * G];
 #pragma unroll
-                for (int l = 0; l < 4; ++l) pk.s[4 * i + l] = w.v[l];
-            } else {
-                float v[4];
-                transform4<DIST>(w, P.p0, P.p1, v);
-#pragma unroll
-                for (int l = 0; l < 4; ++l) pk.s[4 * i + l] = narrow<DT, DIST == BITCAST>(v[l]);
-            }
+            for (int i = 0; i < G; ++i) transform4<DIST>(philox_block(bfirst + i, P.k0, P.k1), P.p0, P.p1, v + 4 * i);
+            pack_narrow<DT, DIST == BITCAST>(v, pk.w);
         }
         const uint64_t j0 = 4 * bfirst - P.offset;
         if (P.vec && j0 + 4 * G <= P.n) {
@@ -271,20 +269,21 @@ __global__ __launch_bounds__(kThreads) void k_gen_packed(PackedParams P)
                     pk.w[i] = wd;
                 }
             } else {
-#pragma unroll
-                for (int e = 0; e < E; ++e) pk.s[e] = narrow<DT, false>(v[e]);
+                pack_narrow<DT, false>(v, pk.w);
             }
         } else {
-            static_assert(W == 16, "normal fields are 16 bits");
+            static_assert(W == 16 && E == 8 * GB, "normal fields are 16 bits, two per word");
+            float v[E];
 #pragma unroll
             for (int i = 0; i < 4 * GB; ++i) {
                 float z0, z1;
                 normal_pair(wv[i] << 16, wv[i] & 0xFFFF0000u, z0, z1);
                 const float s0 = P.p1 * z0;
                 const float s1 = P.p1 * z1;
-                pk.s[2 * i] = narrow<DT, false>(P.p0 + s0);
-                pk.s[2 * i + 1] = narrow<DT, false>(P.p0 + s1);
+                v[2 * i] = P.p0 + s0;
+                v[2 * i + 1] = P.p0 + s1;
             }
+            pack_narrow<DT, false>(v, pk.w);
         }
         const uint64_t q0 = unit * (uint64_t)E;
         if (P.vec && q0 >= P.offset && q0 - P.offset + E <= P.n) {
@@ -374,8 +373,10 @@ __global__ __launch_bounds__(kThreads) void k_xform(XformParams P)
         if (P.vec && j0 + 4 * G <= P.n) {
             union {
                 uint4 v;
+                uint32_t w[4];
                 T s[4 * G];
             } pk;
+            float v[4 * G];
 #pragma unroll
             for (int i = 0; i < G; ++i) {
                 const uint4 raw = reinterpret_cast<const uint4 *>(P.words + j0)[i];
@@ -383,14 +384,12 @@ __global__ __launch_bounds__(kThreads) void k_xform(XformParams P)
                 w.v[0] = raw.x; w.v[1] = raw.y; w.v[2] = raw.z; w.v[3] = raw.w;
                 if constexpr (DT == U32) {
 #pragma unroll
-                    for (int l = 0; l < 4; ++l) pk.s[4 * i + l] = w.v[l];
+                    for (int l = 0; l < 4; ++l) pk.w[l] = w.v[l];
                 } else {
-                    float v[4];
-                    transform4<DIST>(w, P.p0, P.p1, v);
-#pragma unroll
-                    for (int l = 0; l < 4; ++l) pk.s[4 * i + l] = narrow<DT, DIST == BITCAST>(v[l]);
+                    transform4<DIST>(w, P.p0, P.p1, v + 4 * i);
                 }
             }
+            if constexpr (DT != U32) pack_narrow<DT, DIST == BITCAST>(v, pk.w);
             *reinterpret_cast<uint4 *>(P.dst + j0 * ES) = pk.v;
         } else {
             for (int e = 0; e < 4 * G; ++e) {
@@ -781,7 +780,7 @@ struct RatioFilter {
     }
 };
 
-template <int DA, int DB, bool VEC>
+template <int DA, int DB, bool VEC, int D>
 __global__ __launch_bounds__(kThreads) void k_check(const uint8_t *a, const uint8_t *b, uint64_t n, float rtol,
                                                     float atol, CheckPartial *partials, uint32_t U)
 {
@@ -817,39 +816,36 @@ __global__ __launch_bounds__(kThreads) void k_check(const uint8_t *a, const uint
         return cand;
     };
     if constexpr (VEC) {
-        // Software pipeline over two chunk buffers: the loads of the next
-        // chunk are in flight while the current one is evaluated. Every load
-        // is unconditional (a lane with nothing left re-reads its current
-        // chunk, or the last one), so the compiler's memory-counter waits
-        // stay exact: an evaluation waits for its own buffer only, never for
-        // the loads just issued. A lane's chunks only grow with u, so the
-        // first lane of a wave holds a chunk whenever any lane does.
+        // Software pipeline over a ring of D chunk buffers: the loads of the
+        // next D - 1 chunks are in flight while the current one is
+        // evaluated. Every load is unconditional (a lane with nothing left
+        // re-reads the last chunk, which stays in L2), so the compiler's
+        // memory-counter waits stay exact: an evaluation waits for its own
+        // buffer only, never for the loads issued after it. A lane's chunks
+        // only grow with j, so the first lane of a wave holds a chunk
+        // whenever any lane does.
         if (nchunks != 0) {
             const uint64_t last = nchunks - 1;
-            auto step = [&](const typename IO::Raw &r, bool h, uint64_t c) {
-                float A[E], B[E];       // read only where h holds
-                uint64_t cand = 0;
-                if (h) {
-                    IO::widen_raw(r, A, B);
-                    cand = process(A, B, c);
+            auto cj = [&](uint32_t j) { return base + t + (uint64_t)j * kThreads; };
+            auto hj = [&](uint32_t j) { return j < U && cj(j) < nchunks; };
+            typename IO::Raw r[D];
+#pragma unroll
+            for (int k = 0; k < D - 1; ++k) IO::load_raw(a, b, hj(k) ? cj(k) : last, r[k]);
+            for (uint32_t u = 0; u < U; u += D) {
+#pragma unroll
+                for (int k = 0; k < D; ++k) {
+                    const uint32_t jn = u + k + D - 1;
+                    IO::load_raw(a, b, hj(jn) ? cj(jn) : last, r[(k + D - 1) % D]);
+                    const uint32_t j = u + k;
+                    const bool h = hj(j);
+                    float A[E], B[E];   // read only where h holds
+                    uint64_t cand = 0;
+                    if (h) {
+                        IO::widen_raw(r[k], A, B);
+                        cand = process(A, B, cj(j));
+                    }
+                    rf.chunk(A, B, h, cand, acc);
                 }
-                rf.chunk(A, B, h, cand, acc);
-            };
-            typename IO::Raw r0, r1;
-            uint64_t c0 = base + t;
-            bool h0 = c0 < nchunks;
-            IO::load_raw(a, b, h0 ? c0 : last, r0);
-            for (uint32_t u = 0; u < U; u += 2) {
-                const uint64_t c1 = c0 + kThreads;
-                const bool h1 = (u + 1 < U) && c1 < nchunks;
-                IO::load_raw(a, b, h1 ? c1 : (h0 ? c0 : last), r1);
-                step(r0, h0, c0);
-                const uint64_t c2 = c1 + kThreads;
-                const bool h2 = (u + 2 < U) && c2 < nchunks;
-                IO::load_raw(a, b, h2 ? c2 : (h1 ? c1 : last), r0);
-                step(r1, h1, c1);
-                c0 = c2;
-                h0 = h2;
             }
         }
     } else {
@@ -988,9 +984,9 @@ __global__ __launch_bounds__(kFinalThreads) void k_check_final(const CheckPartia
     }
 }
 
-// Blocks of k_check<DA, DB, VEC> the current device holds at once, capped at
-// the partial buffer's capacity; cached per device.
-template <int DA, int DB, bool VEC>
+// Blocks of k_check<DA, DB, VEC, D> the current device holds at once, capped
+// at the partial buffer's capacity; cached per device.
+template <int DA, int DB, bool VEC, int D>
 static uint32_t check_resident()
 {
     constexpr int kDevCache = 64;
@@ -1000,7 +996,7 @@ static uint32_t check_resident()
     if (dev >= 0 && cache[dev]) return cache[dev];
     int per_cu = 0, cus = 0;
     uint32_t r = kMaxCheckBlocks / 2;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_check<DA, DB, VEC>, kThreads, 0) == hipSuccess &&
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_check<DA, DB, VEC, D>, kThreads, 0) == hipSuccess &&
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev < 0 ? 0 : dev) == hipSuccess &&
         per_cu > 0 && cus > 0)
         r = (uint32_t)per_cu * (uint32_t)cus;
@@ -1009,9 +1005,9 @@ static uint32_t check_resident()
     return r;
 }
 
-template <int DA, int DB>
-static hipError_t check_ab(const void *a, const void *b, uint64_t n, float rtol, float atol, void *scratch,
-                           krex_check_result *out, hipStream_t s)
+template <int DA, int DB, int D>
+static hipError_t check_ab_d(const void *a, const void *b, uint64_t n, float rtol, float atol, void *scratch,
+                             krex_check_result *out, hipStream_t s)
 {
     constexpr int SA = dtype_traits<DA>::size, SB = dtype_traits<DB>::size;
     constexpr int E = 16 / (SA < SB ? SA : SB);
@@ -1024,7 +1020,7 @@ static hipError_t check_ab(const void *a, const void *b, uint64_t n, float rtol,
     // the best chunk adds at most 1/8 to the bytes read (and the pipeline
     // has depth).
     static const uint32_t u_floor = tune_env("KREX_CHECK_U", 8);
-    const uint64_t resident = vec ? check_resident<DA, DB, true>() : check_resident<DA, DB, false>();
+    const uint64_t resident = vec ? check_resident<DA, DB, true, D>() : check_resident<DA, DB, false, 2>();
     uint64_t U = (nchunks + (uint64_t)kThreads * resident - 1) / ((uint64_t)kThreads * resident);
     if (U < u_floor) U = u_floor;
     if (U == 0) U = 1;
@@ -1033,13 +1029,27 @@ static hipError_t check_ab(const void *a, const void *b, uint64_t n, float rtol,
     CheckPartial *parts = (CheckPartial *)scratch;
     hipError_t e;
     if (vec)
-        e = launch(k_check<DA, DB, true>, dim3((uint32_t)G), dim3(kThreads), s, (const uint8_t *)a, (const uint8_t *)b,
+        e = launch(k_check<DA, DB, true, D>, dim3((uint32_t)G), dim3(kThreads), s, (const uint8_t *)a, (const uint8_t *)b,
                    n, rtol, atol, parts, (uint32_t)U);
     else
-        e = launch(k_check<DA, DB, false>, dim3((uint32_t)G), dim3(kThreads), s, (const uint8_t *)a,
+        e = launch(k_check<DA, DB, false, 2>, dim3((uint32_t)G), dim3(kThreads), s, (const uint8_t *)a,
                    (const uint8_t *)b, n, rtol, atol, parts, (uint32_t)U);
     if (e != hipSuccess) return e;
     return launch(k_check_final, dim3(1), dim3(kFinalThreads), s, (const CheckPartial *)parts, (uint32_t)G, n, out);
+}
+
+// Depth of the load ring: fp8 pairs evaluate 16 elements per 32 bytes
+// loaded, twice the work per byte of the other pairs, and need a third
+// buffer in flight to keep HBM busy (measured on gfx950: fp8 x fp8 +12%; no
+// gain for the other pairs, whose extra registers only lower occupancy).
+template <int DA, int DB>
+static constexpr int check_depth() { return (DA == F8 && DB == F8) ? 3 : 2; }
+
+template <int DA, int DB>
+static hipError_t check_ab(const void *a, const void *b, uint64_t n, float rtol, float atol, void *scratch,
+                           krex_check_result *out, hipStream_t s)
+{
+    return check_ab_d<DA, DB, check_depth<DA, DB>()>(a, b, n, rtol, atol, scratch, out, s);
 }
 
 template <int DA>
