@@ -573,8 +573,9 @@ hipError_t launch_inject(void *y, const void *x, int dt, uint64_t n, uint64_t ms
 // narrower operand); thread t takes chunk b 256 U + u 256 + t for u < U, so
 // every step of a wave reads contiguous memory. Per element the verdict is
 // branch-free; mismatch and NaN counts are wave ballots summed on the scalar
-// unit; the per-lane maximum |a - b| is tracked per chunk and its first index
-// recovered at the end by re-reading that one chunk. Each block writes one
+// unit; the per-lane maximum |a - b| is tracked per chunk, and the first
+// index of the wave's maximum is recovered at the end by its winning lane
+// re-reading that one chunk. Each block writes one
 // 32-byte partial with plain stores; k_check_final reduces the partials and
 // writes the result record.
 //
@@ -861,14 +862,11 @@ __global__ __launch_bounds__(kThreads) void k_check(const uint8_t *a, const uint
             rf.chunk(A, B, have, cand, acc);
         }
     }
-    // First element of the lane's best chunk attaining best_d.
-    uint64_t best_i = ~0ull;
-    if (best_d >= 0.0f) {
-        float A[E], B[E];
-        IO::load(a, b, best_c, A, B);
-        for (int e = E - 1; e >= 0; --e)
-            if (elem_d(A[e], B[e]) == best_d) best_i = (uint64_t)best_c * E + e;
-    }
+    // The lane's candidate for the |a - b| maximum: best_d at position pos,
+    // the first index of its best chunk (the chunk holds the lane's first
+    // element attaining best_d), or a tail index.
+    uint64_t pos = (uint64_t)best_c * E;
+    bool in_chunk = true;
     // The n mod E tail: the first block's first lanes, one element each.
     const uint64_t tail0 = nchunks * E;
     if (blockIdx.x == 0 && tail0 + t < n) {
@@ -878,11 +876,32 @@ __global__ __launch_bounds__(kThreads) void k_check(const uint8_t *a, const uint
         const float d = check_elem(A, B, rtol, atol, acc);
         if (d > best_d) {     // tail indices exceed every chunk index
             best_d = d;
-            best_i = i;
+            pos = i;
+            in_chunk = false;
         }
     }
+    // Only the wave's winner, the largest best_d at the lowest position,
+    // re-reads its chunk for the exact index (one chunk per wave, not per
+    // lane: a chunk's two operands span two 128-byte lines). Chunks are
+    // disjoint and ordered by position, so no other lane of the wave holds
+    // an element attaining best_d below the winner's chunk, and the exact
+    // key stays the wave's largest.
+    uint64_t key = best_d >= 0.0f ? (((uint64_t)__float_as_uint(best_d) << 33) | (kIdxMask - pos)) : 0ull;
+    uint64_t wkey = key;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const uint64_t k2 = __shfl_xor((unsigned long long)wkey, off, 64);
+        wkey = k2 > wkey ? k2 : wkey;
+    }
+    if (key != 0 && key == wkey && in_chunk) {
+        float A[E], B[E];
+        IO::load(a, b, best_c, A, B);
+        uint64_t best_i = pos;
+        for (int e = E - 1; e >= 0; --e)
+            if (elem_d(A[e], B[e]) == best_d) best_i = pos + (uint64_t)e;
+        key = ((uint64_t)__float_as_uint(best_d) << 33) | (kIdxMask - best_i);
+    }
     float rel = acc.rd / acc.rb;                 // +inf when rb = 0 < rd; 0 for the initial (0, 1)
-    uint64_t key = best_d >= 0.0f ? (((uint64_t)__float_as_uint(best_d) << 33) | (kIdxMask - best_i)) : 0ull;
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
         const uint64_t k2 = __shfl_xor((unsigned long long)key, off, 64);
@@ -1016,9 +1035,8 @@ static hipError_t check_ab_d(const void *a, const void *b, uint64_t n, float rto
     // One resident round: the grid is at most the number of blocks the
     // device holds at once (occupancy x compute units), so no partial last
     // round of blocks idles most of the chip. Chunks per thread: enough to
-    // cover n with that grid, and at least 8 so that the per-lane re-read of
-    // the best chunk adds at most 1/8 to the bytes read (and the pipeline
-    // has depth).
+    // cover n with that grid, and at least u_floor (the pipeline's depth per
+    // lane, and fewer partials for small n).
     static const uint32_t u_floor = tune_env("KREX_CHECK_U", 8);
     const uint64_t resident = vec ? check_resident<DA, DB, true, D>() : check_resident<DA, DB, false, 2>();
     uint64_t U = (nchunks + (uint64_t)kThreads * resident - 1) / ((uint64_t)kThreads * resident);
