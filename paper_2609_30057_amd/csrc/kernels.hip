@@ -23,7 +23,11 @@
 // shape never changes a result: every element's value depends only on its
 // index.
 #include <hip/hip_runtime.h>
+#include <float.h>
+#include <math.h>
 #include <stdlib.h>
+
+#include <cmath>
 
 #include <tuple>
 #include <utility>
@@ -59,6 +63,8 @@ struct GenParams {
     uint64_t offset;
     uint32_t k0, k1;
     float p0, p1;      // uniform: lo and fl(hi - lo); normal: mean and std
+    float c;           // uniform with a power-of-two range: range 2^-24
+    int pow2;          // uniform range is a power of two (c normal)
     uint64_t b0;       // first Philox block
     uint64_t ngroups;  // groups of G blocks
     uint32_t U;        // groups per thread, block-contiguous
@@ -85,9 +91,17 @@ __global__ __launch_bounds__(kThreads) void k_gen(GenParams P)
 #pragma unroll
             for (int l = 0; l < 4; ++l) pk.w[l] = w.v[l];
         } else {
-            float v[4 * G];
+            words4 wb[G];
 #pragma unroll
-            for (int i = 0; i < G; ++i) transform4<DIST>(philox_block(bfirst + i, P.k0, P.k1), P.p0, P.p1, v + 4 * i);
+            for (int i = 0; i < G; ++i) wb[i] = philox_block(bfirst + i, P.k0, P.k1);
+            float v[4 * G];
+            if (DIST == UNIFORM && P.pow2) {     // uniform across the launch
+#pragma unroll
+                for (int i = 0; i < G; ++i) transform4<DIST, true>(wb[i], P.p0, P.c, v + 4 * i);
+            } else {
+#pragma unroll
+                for (int i = 0; i < G; ++i) transform4<DIST>(wb[i], P.p0, P.p1, v + 4 * i);
+            }
             pack_narrow<DT, DIST == BITCAST>(v, pk.w);
         }
         const uint64_t j0 = 4 * bfirst - P.offset;
@@ -125,6 +139,23 @@ static uint32_t tune_env(const char *name, uint32_t dflt)
     return v ? (uint32_t)v : dflt;
 }
 
+// Whether range 2^-W times every integer f in [0, 2^W) is an exact fp32
+// product: range positive and finite, range 2^-W normal, and range's 24-bit
+// significand ending in at least W zero bits (W = 24: a power of two). Then
+// lo + fl(range 2^-W f) equals the single fused multiply-add. *c = range 2^-W.
+static bool exact_scale(float range, int W, float *c)
+{
+    *c = 0.0f;
+    if (!(range > 0.0f) || !std::isfinite(range)) return false;
+    int e = 0;
+    const float m = frexpf(range, &e);                       // m in [1/2, 1)
+    const uint32_t sig = (uint32_t)ldexpf(m, 24);             // exact 24-bit significand
+    const float cc = ldexpf(range, -W);
+    if (!(cc >= FLT_MIN) || (uint32_t)__builtin_ctz(sig) < (uint32_t)W) return false;
+    *c = cc;
+    return true;
+}
+
 template <int DT, int DIST>
 static hipError_t gen_dt_dist(GenParams P, hipStream_t s)
 {
@@ -157,6 +188,7 @@ hipError_t launch_gen(void *dst, int dt, uint64_t n, uint64_t seed, uint64_t off
     P.k1 = (uint32_t)(seed >> 32);
     P.p0 = p0;
     P.p1 = (dist == UNIFORM) ? (p1 - p0) : p1;
+    P.pow2 = (dist == UNIFORM && exact_scale(P.p1, 24, &P.c)) ? 1 : 0;
     P.b0 = offset >> 2;
     const uint64_t blast = (offset + (n - 1)) >> 2;
     const uint64_t nblocks = blast - P.b0 + 1;
@@ -205,6 +237,7 @@ struct PackedParams {
     float p0, p1;      // uniform: lo and fl(hi - lo); normal: mean and std
     float rs;          // uniform: fl(hi - lo) 2^-W when that is exact
     int scaled;        // rs is exact
+    int fused;         // also rs f exact for every field f: one fused multiply-add
     uint64_t u0;       // first unit (units are E fields, E-aligned)
     uint64_t nunits;
     uint32_t U;        // units per thread, block-contiguous
@@ -243,7 +276,14 @@ __global__ __launch_bounds__(kThreads) void k_gen_packed(PackedParams P)
             for (int l = 0; l < 4; ++l) pk.w[l] = wv[l];
         } else if constexpr (DIST == UNIFORM) {
             float v[E];
-            if (P.scaled) {
+            if (P.fused) {
+                // rs f is exact as well: lo + rs f has one rounding.
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    const uint32_t f = (wv[e / K] >> ((e % K) * W)) & kMask;
+                    v[e] = __builtin_fmaf(P.rs, (float)f, P.p0);
+                }
+            } else if (P.scaled) {
                 // u = f 2^-W exactly, and rs = fl(hi - lo) 2^-W exactly, so
                 // the product rs f is the same real number as fl(hi - lo) u
                 // and rounds the same: one conversion, one multiply, one add.
@@ -306,9 +346,12 @@ static hipError_t gen_packed_dt_dist(PackedParams P, hipStream_t s)
     if (DIST == UNIFORM) {
         P.rs = ldexpf(P.p1, -W);
         P.scaled = (ldexpf(P.rs, W) == P.p1) ? 1 : 0;
+        float c;
+        P.fused = (P.scaled && exact_scale(P.p1, W, &c)) ? 1 : 0;
     } else {
         P.rs = 0.0f;
         P.scaled = 0;
+        P.fused = 0;
     }
     P.u0 = P.offset / E;
     P.nunits = (P.offset + (P.n - 1)) / E - P.u0 + 1;
@@ -355,6 +398,8 @@ struct XformParams {
     const uint32_t *words;
     uint64_t n;
     float p0, p1;
+    float c;           // as in GenParams
+    int pow2;
     uint64_t ngroups;
     uint32_t U;
     int vec;
@@ -385,6 +430,8 @@ __global__ __launch_bounds__(kThreads) void k_xform(XformParams P)
                 if constexpr (DT == U32) {
 #pragma unroll
                     for (int l = 0; l < 4; ++l) pk.w[l] = w.v[l];
+                } else if (DIST == UNIFORM && P.pow2) {
+                    transform4<DIST, true>(w, P.p0, P.c, v + 4 * i);
                 } else {
                     transform4<DIST>(w, P.p0, P.p1, v + 4 * i);
                 }
@@ -401,7 +448,7 @@ __global__ __launch_bounds__(kThreads) void k_xform(XformParams P)
                 } else {
                     float v;
                     if constexpr (DIST == UNIFORM) {
-                        v = uniform_f32(P.words[j], P.p0, P.p1);
+                        v = P.pow2 ? uniform_f32_pow2(P.words[j], P.p0, P.c) : uniform_f32(P.words[j], P.p0, P.p1);
                     } else if constexpr (DIST == NORMAL) {
                         float z0, z1;
                         normal_pair(P.words[j & ~(uint64_t)1], P.words[j | 1u], z0, z1);
@@ -441,6 +488,7 @@ hipError_t launch_xform(void *dst, int dt, uint64_t n, const uint32_t *words, in
     P.n = n;
     P.p0 = p0;
     P.p1 = (dist == UNIFORM) ? (p1 - p0) : p1;
+    P.pow2 = (dist == UNIFORM && exact_scale(P.p1, 24, &P.c)) ? 1 : 0;
     const int G = (dt == BF16 || dt == F16) ? 2 : (dt == F8 ? 4 : 1);
     P.ngroups = (n + 4u * G - 1) / (4u * G);
     P.vec = (((uintptr_t)dst & 15u) == 0 && ((uintptr_t)words & 15u) == 0) ? 1 : 0;

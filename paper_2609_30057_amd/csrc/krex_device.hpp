@@ -373,13 +373,23 @@ __device__ __forceinline__ float uniform_f32(uint32_t w, float lo, float range)
     return lo + t;
 }
 
-// Four values from four consecutive words (two normal pairs).
-template <int DIST>
+// The uniform transform when range = fl(hi - lo) is a power of two with
+// c = range 2^-24 normal: range u = c (w >> 8) is then exact (a 24-bit
+// integer times a power of two), so lo + fl(range u) has a single rounding
+// and one fused multiply-add gives the same value.
+__device__ __forceinline__ float uniform_f32_pow2(uint32_t w, float lo, float c)
+{
+    return __builtin_fmaf(c, (float)(w >> 8), lo);
+}
+
+// Four values from four consecutive words (two normal pairs). POW2: the
+// uniform range is a power of two and p1 holds c = range 2^-24.
+template <int DIST, bool POW2 = false>
 __device__ __forceinline__ void transform4(const words4 &w, float p0, float p1, float v[4])
 {
     if constexpr (DIST == UNIFORM) {
 #pragma unroll
-        for (int l = 0; l < 4; ++l) v[l] = uniform_f32(w.v[l], p0, p1);
+        for (int l = 0; l < 4; ++l) v[l] = POW2 ? uniform_f32_pow2(w.v[l], p0, p1) : uniform_f32(w.v[l], p0, p1);
     } else if constexpr (DIST == NORMAL) {
         float z[4];
         normal_pair(w.v[0], w.v[1], z[0], z[1]);

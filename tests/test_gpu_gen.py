@@ -13,7 +13,11 @@ from tests.gpu_helpers import assert_bits_equal, empty, from_storage, to_storage
 pytestmark = pytest.mark.gpu
 
 DTS = ["f32", "bf16", "f16", "f8"]
-DISTS = [(0, -1.0, 1.0), (0, -4.0, 4.0), (0, 0.1, 0.7), (1, 0.0, 1.0), (1, 2.5, 0.5), (2, 0.0, 0.0)]
+# Uniform ranges: powers of two (-1..1, -4..4, 1000..1016: one fused
+# multiply-add in the kernel), 2^-110 (a power of two whose 2^-24 step would
+# be subnormal) and 0.6 take the two-rounding path.
+DISTS = [(0, -1.0, 1.0), (0, -4.0, 4.0), (0, 0.1, 0.7), (1, 0.0, 1.0), (1, 2.5, 0.5), (2, 0.0, 0.0),
+         (0, 1000.0, 1016.0), (0, 0.0, 2.0**-110)]
 SIZES = [0, 1, 3, 15, 17, 4099, (1 << 20) + 5]
 OFFSETS = [0, 1, 3, 65536, 4 * (2**32 - 1) - 6]
 SEEDS = [0, 2**64 - 1]
@@ -100,7 +104,7 @@ def test_uniform_transform_all_24bit_values():
     k = np.arange(1 << 24, dtype=np.uint32) << 8
     words = from_storage(k, "u32")
     for dt in DTS:
-        for lo, hi in ((-1.0, 1.0), (0.1, 0.7), (-4.0, 4.0)):
+        for lo, hi in ((-1.0, 1.0), (0.1, 0.7), (-4.0, 4.0), (1000.0, 1016.0)):
             t = empty(dt, k.size)
             krex.transform_words(t, words, "uniform", lo, hi)
             assert_bits_equal(to_storage(t, dt), oracle.transform_words(dt, k, 0, lo, hi), "%s uniform" % dt)
