@@ -23,6 +23,8 @@ Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
        python bench.py --configs          the other commands: gemm_tiny, check_stress, mixed_stream
        python bench.py --calib-copy       also time a plain 1 GiB device copy (the
                                           reference kernel for rocprofv3 byte counters)
+       python bench.py --valu-rates       issue cost of the vector instructions the kernels
+                                          use (cycles per wave64 instruction per SIMD)
 """
 import argparse
 import json
@@ -410,6 +412,7 @@ def main():
     ap.add_argument("--kernels", action="store_true")
     ap.add_argument("--calib-copy", action="store_true")
     ap.add_argument("--configs", action="store_true")
+    ap.add_argument("--valu-rates", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (use --gpus 1)", file=sys.stderr)
@@ -426,6 +429,12 @@ def main():
     if args.configs:
         print(json.dumps(run_configs()), flush=True)
         return
+    if args.valu_rates:
+        import subprocess
+        exe = os.path.join(ROOT, "paper_2609_30057_amd", "valu_rates")
+        if not os.path.exists(exe):
+            raise SystemExit("valu_rates is not built; run __graft_entry__.build()")
+        sys.exit(subprocess.run([exe]).returncode)
     out = run_gemm_large(args.steps, args.warmup, not args.no_cpu_baseline)
     if args.calib_copy:
         run_copy_calibration()

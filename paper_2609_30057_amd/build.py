@@ -7,6 +7,9 @@
   libkrex_intercept.so the ROCm tools library of include/krex_intercept.h
                        (loaded through HSA_TOOLS_LIB).
 
+and the measurement program valu_rates (issue cost of the vector
+instructions the kernels use, run by bench.py --valu-rates).
+
 kernels.hip is compiled as HIP for --offload-arch=gfx950; the rest is host
 C++. Floating-point flags fix the semantics
 the generated values and check verdicts are defined with: no contraction
@@ -26,6 +29,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libkrex.so")
 GATE_LIB = os.path.join(HERE, "libkrexgate.so")
 INTERCEPT_LIB = os.path.join(HERE, "libkrex_intercept.so")
+VALU_RATES = os.path.join(HERE, "valu_rates")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
@@ -74,7 +78,25 @@ def build(verbose: bool = False) -> str:
     _link(GATE_LIB, [gate], ["-Wl,-soname,libkrexgate.so", "-lpthread", "-lrt"], verbose, linker="g++")
     _link(LIB, [kernels, api], ["--offload-arch=" + ARCH, *rpath], verbose)
     _link(INTERCEPT_LIB, [intercept], rpath, verbose, linker="g++")
+    tmp = VALU_RATES + ".tmp%d" % os.getpid()
+    cmd = [HIPCC, "-O3", "-std=c++17", "-x", "hip", "--offload-arch=" + ARCH, "-Xclang", "-target-feature",
+           "-Xclang", "-packed-fp32-ops", os.path.join(CSRC, "valu_rates.hip"), "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("compile failed: %s\n%s%s" % (" ".join(cmd), r.stdout, r.stderr))
+    os.replace(tmp, VALU_RATES)
     return LIB
+
+
+def emit_asm(out_path: str) -> str:
+    """gfx950 assembly of kernels.hip with the library's device flags."""
+    cmd = [HIPCC, *COMMON, *DEVICE, "--cuda-device-only", "-S", os.path.join(CSRC, "kernels.hip"), "-o", out_path]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("compile failed: %s\n%s%s" % (" ".join(cmd), r.stdout, r.stderr))
+    return out_path
 
 
 if __name__ == "__main__":

@@ -71,7 +71,8 @@ struct GenParams {
     int vec;           // offset % 4 == 0 and dst 16-byte aligned
 };
 
-template <int DT, int DIST>
+// POW2: uniform with a power-of-two range (the fused transform; P.c).
+template <int DT, int DIST, bool POW2>
 __global__ __launch_bounds__(kThreads) void k_gen(GenParams P)
 {
     using T = typename dtype_traits<DT>::storage;
@@ -95,13 +96,8 @@ __global__ __launch_bounds__(kThreads) void k_gen(GenParams P)
 #pragma unroll
             for (int i = 0; i < G; ++i) wb[i] = philox_block(bfirst + i, P.k0, P.k1);
             float v[4 * G];
-            if (DIST == UNIFORM && P.pow2) {     // uniform across the launch
 #pragma unroll
-                for (int i = 0; i < G; ++i) transform4<DIST, true>(wb[i], P.p0, P.c, v + 4 * i);
-            } else {
-#pragma unroll
-                for (int i = 0; i < G; ++i) transform4<DIST>(wb[i], P.p0, P.p1, v + 4 * i);
-            }
+            for (int i = 0; i < G; ++i) transform4<DIST, POW2>(wb[i], P.p0, POW2 ? P.c : P.p1, v + 4 * i);
             pack_narrow<DT, DIST == BITCAST>(v, pk.w);
         }
         const uint64_t j0 = 4 * bfirst - P.offset;
@@ -140,9 +136,11 @@ static uint32_t tune_env(const char *name, uint32_t dflt)
 }
 
 // Whether range 2^-W times every integer f in [0, 2^W) is an exact fp32
-// product: range positive and finite, range 2^-W normal, and range's 24-bit
-// significand ending in at least W zero bits (W = 24: a power of two). Then
-// lo + fl(range 2^-W f) equals the single fused multiply-add. *c = range 2^-W.
+// product: range positive and finite, c = range 2^-W normal, and the odd part
+// q of range's 24-bit significand small enough that f q < 2^24 for every f
+// (range = q 2^s, so f c = f q 2^(s - W) is then a 24-bit integer times a
+// power of two, at least c, hence a normal float). W = 24 with q = 1: a power
+// of two. Then lo + fl(c f) equals the single fused multiply-add. *c = c.
 static bool exact_scale(float range, int W, float *c)
 {
     *c = 0.0f;
@@ -150,8 +148,9 @@ static bool exact_scale(float range, int W, float *c)
     int e = 0;
     const float m = frexpf(range, &e);                       // m in [1/2, 1)
     const uint32_t sig = (uint32_t)ldexpf(m, 24);             // exact 24-bit significand
+    const uint64_t q = sig >> __builtin_ctz(sig);
     const float cc = ldexpf(range, -W);
-    if (!(cc >= FLT_MIN) || (uint32_t)__builtin_ctz(sig) < (uint32_t)W) return false;
+    if (!(cc >= FLT_MIN) || q * ((1ull << W) - 1ull) >= (1ull << 24)) return false;
     *c = cc;
     return true;
 }
@@ -162,7 +161,9 @@ static hipError_t gen_dt_dist(GenParams P, hipStream_t s)
     static const uint32_t u_pref = tune_env("KREX_GEN_U", 1);
     uint32_t grid;
     shape(P.ngroups, u_pref, &P.U, &grid);
-    return launch(k_gen<DT, DIST>, dim3(grid), dim3(kThreads), s, P);
+    if constexpr (DIST == UNIFORM && DT != U32)
+        if (P.pow2) return launch(k_gen<DT, DIST, true>, dim3(grid), dim3(kThreads), s, P);
+    return launch(k_gen<DT, DIST, false>, dim3(grid), dim3(kThreads), s, P);
 }
 
 template <int DT>
@@ -236,15 +237,21 @@ struct PackedParams {
     uint32_t k0, k1;
     float p0, p1;      // uniform: lo and fl(hi - lo); normal: mean and std
     float rs;          // uniform: fl(hi - lo) 2^-W when that is exact
-    int scaled;        // rs is exact
-    int fused;         // also rs f exact for every field f: one fused multiply-add
+    int umode;         // uniform: UM_WORD, UM_SCALED or UM_FUSED
     uint64_t u0;       // first unit (units are E fields, E-aligned)
     uint64_t nunits;
     uint32_t U;        // units per thread, block-contiguous
     int vec;           // offset % E == 0 and dst 16-byte aligned
 };
 
-template <int DT, int DIST>
+// Uniform transform of a W-bit field f: UM_WORD applies the word-stream
+// transform to f << (32 - W); UM_SCALED when rs = fl(hi - lo) 2^-W is exact
+// (u = f 2^-W exactly, so rs f is the same real number as fl(hi - lo) u and
+// rounds the same: one conversion, one multiply, one add); UM_FUSED when rs f
+// is exact as well, so lo + rs f has one rounding: one fused multiply-add.
+enum : int { UM_WORD = 0, UM_SCALED = 1, UM_FUSED = 2 };
+
+template <int DT, int DIST, int UM>
 __global__ __launch_bounds__(kThreads) void k_gen_packed(PackedParams P)
 {
     using T = typename dtype_traits<DT>::storage;
@@ -276,27 +283,15 @@ __global__ __launch_bounds__(kThreads) void k_gen_packed(PackedParams P)
             for (int l = 0; l < 4; ++l) pk.w[l] = wv[l];
         } else if constexpr (DIST == UNIFORM) {
             float v[E];
-            if (P.fused) {
-                // rs f is exact as well: lo + rs f has one rounding.
 #pragma unroll
-                for (int e = 0; e < E; ++e) {
-                    const uint32_t f = (wv[e / K] >> ((e % K) * W)) & kMask;
+            for (int e = 0; e < E; ++e) {
+                const uint32_t f = (wv[e / K] >> ((e % K) * W)) & kMask;
+                if constexpr (UM == UM_FUSED) {
                     v[e] = __builtin_fmaf(P.rs, (float)f, P.p0);
-                }
-            } else if (P.scaled) {
-                // u = f 2^-W exactly, and rs = fl(hi - lo) 2^-W exactly, so
-                // the product rs f is the same real number as fl(hi - lo) u
-                // and rounds the same: one conversion, one multiply, one add.
-#pragma unroll
-                for (int e = 0; e < E; ++e) {
-                    const uint32_t f = (wv[e / K] >> ((e % K) * W)) & kMask;
+                } else if constexpr (UM == UM_SCALED) {
                     const float t = P.rs * (float)f;
                     v[e] = P.p0 + t;
-                }
-            } else {
-#pragma unroll
-                for (int e = 0; e < E; ++e) {
-                    const uint32_t f = (wv[e / K] >> ((e % K) * W)) & kMask;
+                } else {
                     v[e] = uniform_f32(f << (32 - W), P.p0, P.p1);
                 }
             }
@@ -343,22 +338,23 @@ static hipError_t gen_packed_dt_dist(PackedParams P, hipStream_t s)
 {
     constexpr int E = packed_of<DT, DIST>::E;
     constexpr int W = packed_of<DT, DIST>::W;
+    P.umode = UM_WORD;
+    P.rs = 0.0f;
     if (DIST == UNIFORM) {
         P.rs = ldexpf(P.p1, -W);
-        P.scaled = (ldexpf(P.rs, W) == P.p1) ? 1 : 0;
         float c;
-        P.fused = (P.scaled && exact_scale(P.p1, W, &c)) ? 1 : 0;
-    } else {
-        P.rs = 0.0f;
-        P.scaled = 0;
-        P.fused = 0;
+        if (ldexpf(P.rs, W) == P.p1) P.umode = exact_scale(P.p1, W, &c) ? UM_FUSED : UM_SCALED;
     }
     P.u0 = P.offset / E;
     P.nunits = (P.offset + (P.n - 1)) / E - P.u0 + 1;
     P.vec = (P.offset % E == 0 && ((uintptr_t)P.dst & 15u) == 0) ? 1 : 0;
     uint32_t grid;
     shape(P.nunits, 1, &P.U, &grid);
-    return launch(k_gen_packed<DT, DIST>, dim3(grid), dim3(kThreads), s, P);
+    if constexpr (DIST == UNIFORM) {
+        if (P.umode == UM_FUSED) return launch(k_gen_packed<DT, DIST, UM_FUSED>, dim3(grid), dim3(kThreads), s, P);
+        if (P.umode == UM_SCALED) return launch(k_gen_packed<DT, DIST, UM_SCALED>, dim3(grid), dim3(kThreads), s, P);
+    }
+    return launch(k_gen_packed<DT, DIST, UM_WORD>, dim3(grid), dim3(kThreads), s, P);
 }
 
 template <int DT>

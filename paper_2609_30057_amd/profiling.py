@@ -3,10 +3,23 @@
   python -m paper_2609_30057_amd.profiling stats  --csv DIR/..._kernel_stats.csv --out FILE.md --cmd "..."
   python -m paper_2609_30057_amd.profiling traffic --fetch DIR --write DIR --out-json profiles/traffic.json
                                                  --out FILE.md --cmd "..."
+  python -m paper_2609_30057_amd.profiling valu-model --rates RATES.json --trace DIR/..._kernel_trace.csv
+                                                 --out FILE.md --cmd "..."
+
+valu-model: for the one-unit-per-thread kernels (generation), the vector
+instructions of the per-unit path in the gfx950 assembly (from the loop head
+to the 16-byte store), each weighted by its measured issue cost (cycles per
+wave64 instruction, bench.py --valu-rates), times the waves of the launch in
+the kernel trace, over 4 SIMDs per CU x CUs x 2.4 GHz: the time the launch
+needs at full vector issue, compared with its measured duration.
 
 traffic: per-dispatch FETCH_SIZE and WRITE_SIZE (KiB) of each kernel, scaled by
 what the same counters read for a plain device copy of 1 GiB (1 GiB fetched,
-1 GiB written), and compared with the kernel's algorithmic bytes.
+1 GiB written), and compared with the kernel's algorithmic bytes. With
+--rdreq, a third pass of the read-request counters by size
+(TCC_EA0_RDREQ_32B/64B/128B) gives the bytes read exactly: on gfx950
+FETCH_SIZE counts a 128-byte request as 64 bytes, so the copy's factor of 2
+is only right for kernels whose reads are all 128-byte requests.
 """
 import argparse
 import csv
@@ -94,6 +107,11 @@ def cmd_traffic(a):
     w_copy = statistics.median(write[ck]) * 1024.0
     sf, sw = GIB / f_copy, GIB / w_copy
     algo = json.loads(a.algo) if a.algo else {}
+    exact = {}
+    if a.rdreq:
+        parts = {sz: counters(a.rdreq, "TCC_EA0_RDREQ_%dB_sum" % sz) for sz in (32, 64, 128)}
+        for k in parts[128]:
+            exact[k] = sum(sz * statistics.median(parts[sz].get(k, [0.0])) for sz in (32, 64, 128))
     data = {"calibration": {"kernel": _short(ck), "fetch_bytes": f_copy, "write_bytes": w_copy,
                             "fetch_scale": sf, "write_scale": sw}}
     lines = ["# HBM traffic per dispatch (rocprofv3 FETCH_SIZE / WRITE_SIZE): %s" % a.title, "",
@@ -101,18 +119,26 @@ def cmd_traffic(a):
              "Calibration: `%s`, a plain 1 GiB device copy, reads FETCH %.0f MiB and WRITE %.0f MiB; "
              "scale factors %.4f (fetch) and %.4f (write) turn counter bytes into HBM bytes." % (
                  _short(ck), f_copy / 2**20, w_copy / 2**20, sf, sw), "",
-             "| Kernel | Dispatches | FETCH (MiB, scaled) | WRITE (MiB, scaled) | Algorithmic (MiB) | Traffic / algorithmic |",
-             "|---|---|---|---|---|---|"]
+             "| Kernel | Dispatches | FETCH (MiB, scaled) | Read by request size (MiB) | WRITE (MiB, scaled) "
+             "| Algorithmic (MiB) | Traffic / algorithmic |",
+             "|---|---|---|---|---|---|---|"]
+    if a.rdreq:
+        cr = exact.get(ck)
+        lines[-4] += (" The read-request counters by size give the copy %.1f MiB read (1024 expected)." % (cr / 2**20)
+                      if cr else " The copy kernel is missing from the read-request pass.")
     for k in sorted(fetch):
         if not k.startswith(("krex", "void krex")):
             continue
         fb = statistics.median(fetch[k]) * 1024.0 * sf
         wb = statistics.median(write.get(k, [0.0])) * 1024.0 * sw
+        rb = exact.get(k)
         key = _short(k)
         al = algo.get(key)
-        lines.append("| `%s` | %d | %.1f | %.1f | %s | %s |" % (
-            key, len(fetch[k]), fb / 2**20, wb / 2**20, "%.1f" % (al / 2**20) if al else "-",
-            "%.3f" % ((fb + wb) / al) if al else "-"))
+        rd = rb if rb is not None else fb
+        lines.append("| `%s` | %d | %.1f | %s | %.1f | %s | %s |" % (
+            key, len(fetch[k]), fb / 2**20, "%.1f" % (rb / 2**20) if rb is not None else "-", wb / 2**20,
+            "%.1f" % (al / 2**20) if al else "-", "%.3f" % ((rd + wb) / al) if al else "-"))
+        fb = rd
         short = key.split("::")[-1].split("<")[0]
         data["%s/%s" % (short, a.workload)] = {
             "kernel": key, "hbm_bytes_per_launch": round(fb + wb), "fetch_bytes": round(fb), "write_bytes": round(wb),
@@ -121,6 +147,84 @@ def cmd_traffic(a):
         f.write("\n".join(lines) + "\n")
     with open(a.out_json, "w") as f:
         json.dump(data, f, indent=1)
+
+
+def _unit_path(asm, kernel_symbol):
+    """Vector instructions of `kernel_symbol`'s per-unit path: from the loop
+    head to the first 16-byte store."""
+    m = re.search(r"^" + re.escape(kernel_symbol) + r":(.*?)\.Lfunc_end", asm, re.S | re.M)
+    if not m:
+        raise KeyError(kernel_symbol)
+    body = m.group(1).splitlines()
+    start = next(i for i, l in enumerate(body) if "Loop Header" in l)
+    end = next(i for i, l in enumerate(body) if "global_store_dwordx4" in l)
+    ops = []
+    for l in body[start:end + 1]:
+        t = l.strip()
+        if t and not t.startswith((".", ";")) and not l.startswith("."):
+            ops.append(t.split()[0])
+    return [o for o in ops if o.startswith("v_")]
+
+
+def _op_cost(op, rates):
+    base = re.sub(r"_e(32|64)$|_sdwa$|_dpp$", "", op)
+    if base in rates:
+        return rates[base]
+    for prefix, ref in (("v_cmp", "v_cmp_lt_f32"), ("v_cvt_pk_fp8", "v_cvt_pk_fp8_f32"), ("v_cvt_pk_bf16", "v_cvt_pk_bf16_f32"),
+                        ("v_cvt_pk_f16", "v_cvt_pk_f16_f32"), ("v_cvt", "v_cvt_f32_u32"), ("v_fmac", "v_fma_f32"),
+                        ("v_fmamk", "v_fmaak_f32"), ("v_fma", "v_fma_f32"), ("v_sub_f32", "v_add_f32"),
+                        ("v_sub_u32", "v_add_u32"), ("v_add_", "v_add_u32"), ("v_min3", "v_max3_f32"),
+                        ("v_min", "v_max_f32"), ("v_max", "v_max_f32"), ("v_or", "v_and_b32"), ("v_xor", "v_and_b32"),
+                        ("v_lshl", "v_lshrrev_b32"), ("v_lshr", "v_lshrrev_b32"), ("v_mul_f32", "v_mul_f32"),
+                        ("v_mov", "v_and_b32"), ("v_rcp", "v_rcp_f32"), ("v_sqrt", "v_sqrt_f32"),
+                        ("v_mad_u64", "v_mad_u64_u32"), ("v_mul_hi", "v_mul_hi_u32"), ("v_perm", "v_perm_b32")):
+        if base.startswith(prefix):
+            return rates[ref]
+    return 4.0   # unmeasured: the half-rate cost most conversions and 64-bit operations have
+
+
+def cmd_valu_model(a):
+    from paper_2609_30057_amd import build as B
+    rates = json.load(open(a.rates))["cycles"]
+    asm_path = B.emit_asm(os.path.join(B.BUILD, "kernels.s"))
+    asm = open(asm_path).read()
+    trace = _rows(a.trace)
+    launches = {}
+    for r in trace:
+        name = _short(r["Kernel_Name"])
+        if not name.startswith(("krex::k_gen<", "krex::k_gen_packed<")):
+            continue
+        dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        grid = int(r.get("Grid_Size") or r["Grid_Size_X"])
+        launches.setdefault(name, []).append((grid, dur))
+    clock = 2.4e9
+    lines = ["# Vector-issue roofline of the generation kernels: %s" % a.title, "",
+             "Commands (from the repository root):", "", "    " + a.cmd.replace(" ;; ", "\n    "), "",
+             "Per unit (one thread, one 16-byte output vector) the kernel runs the vector instructions of its "
+             "unit path; each costs its measured issue cycles per wave64 instruction (v_fma_f32 = 2). The launch "
+             "needs waves x weighted cycles / (4 SIMDs x %d CUs x 2.4 GHz) at full vector issue." % a.cus, "",
+             "Each unit also writes one 16-byte vector: grid x 16 bytes at 8 TB/s is the launch's HBM time. The "
+             "larger of the two times bounds the kernel.", "",
+             "| Kernel | Vector instr. per unit | Weighted cycles per wave | Waves | Time at full issue (us) "
+             "| HBM time (us) | Bound | Measured (us) | Fraction of the bound |", "|---|---|---|---|---|---|---|---|---|"]
+    for name in sorted(launches):
+        args = re.match(r"krex::k_gen(?:_packed)?<(.*)>", name).group(1).split(", ")
+        if "packed" in name:
+            sym = "_ZN4krex12k_gen_packedILi%sELi%sELi%sEEEvNS_12PackedParamsE" % tuple(args)
+        else:
+            sym = "_ZN4krex5k_genILi%sELi%sELb%dEEEvNS_9GenParamsE" % (args[0], args[1], args[2] == "true")
+        ops = _unit_path(asm, sym)
+        cyc = sum(_op_cost(o, rates) for o in ops)
+        grid, _ = max(launches[name])
+        durs = [d for g, d in launches[name] if g == grid]
+        meas = statistics.median(durs)
+        waves = grid / 64.0
+        t = waves * cyc / (4 * a.cus * clock) * 1e6
+        th = grid * 16 / 8e12 * 1e6
+        lines.append("| `%s` | %d | %.0f | %d | %.1f | %.1f | %s | %.1f | %.2f |" % (
+            name, len(ops), cyc, waves, t, th, "issue" if t >= th else "HBM", meas, max(t, th) / meas))
+    with open(a.out, "w") as f:
+        f.write("\n".join(lines) + "\n")
 
 
 def main():
@@ -140,11 +244,21 @@ def main():
     t.add_argument("--title", default="")
     t.add_argument("--workload", default="gemm_large")
     t.add_argument("--algo", default="", help="JSON {kernel: algorithmic bytes per launch}")
+    t.add_argument("--rdreq", default="", help="directory of the read-request-size counter pass")
+    v = sub.add_parser("valu-model")
+    v.add_argument("--rates", required=True)
+    v.add_argument("--trace", required=True)
+    v.add_argument("--out", required=True)
+    v.add_argument("--cmd", required=True)
+    v.add_argument("--title", default="")
+    v.add_argument("--cus", type=int, default=256)
     a = ap.parse_args()
     if a.cmd_name == "stats":
         cmd_stats(a)
-    else:
+    elif a.cmd_name == "traffic":
         cmd_traffic(a)
+    else:
+        cmd_valu_model(a)
 
 
 if __name__ == "__main__":
