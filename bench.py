@@ -278,7 +278,62 @@ def run_kernels():
             "peak_GBps": HBM_PEAK_GBPS, "kernels": res}
 
 
-def run_configs():
+def configs_cpu_baseline(cmds):
+    """The oracle (single-threaded C) on bounded samples of the other commands,
+    with the same byte accounting as the GPU figures."""
+    import numpy as np
+    import oracle
+    from paper_2609_30057_amd import workloads as W
+    out = {}
+
+    def t(fn):
+        t0 = time.perf_counter()
+        r = fn()
+        return time.perf_counter() - t0, r
+
+    def flush_s(nbytes, reps, sample):
+        buf = np.zeros(nbytes // 4, dtype=np.uint32)
+        oracle.flush_fill(buf, 1)                          # first touch, not timed
+        dt, _ = t(lambda: [oracle.flush_fill(buf, (0x9E3779B9 * (r + 1)) & 0xFFFFFFFF) for r in range(sample)])
+        return dt * reps / sample
+
+    cfg = W.GEMM_TINY
+    n2 = cfg["n"] * cfg["n"]
+    offA, offB = W.gemm_tiny_offsets()
+    tg, (A, B) = t(lambda: (oracle.gen("f32", n2, cfg["seed"], offA), oracle.gen("f32", n2, cfg["seed"], offB)))
+    tc, _ = t(lambda: oracle.check(A, "f32", B, "f32", cfg["rtol"], cfg["atol"]))
+    tf = flush_s(cfg["flush_bytes"], cfg["reps"], 10)
+    nbytes = 2 * n2 * 4 + n2 * 8 + cfg["reps"] * cfg["flush_bytes"]
+    out["gemm_tiny"] = {"value": round(nbytes / (tg + tc + tf) / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+                        "sample": "both matrices, one 65,536-element fp32 check, 10 of the 100 512 MiB flush fills "
+                                  "scaled x10"}
+    cfg = W.CHECK_STRESS
+    m = cfg["rows"] * cfg["cols"] // 8
+    tg, x = t(lambda: oracle.gen("f16", m, cfg["seed"], 0, 0, cfg["p0"], cfg["p1"]))
+    ti, (y, _) = t(lambda: oracle.inject(x, "f16", cfg["mask_seed"], cfg["rate"], cfg["delta"], oracle.INJ_EXACT))
+    tc, _ = t(lambda: oracle.check(y, "f16", x, "f16", cfg["rtol"], cfg["atol"]))
+    out["check_stress"] = {"value": round(m * 10 / (tg + ti + tc) / 1e9, 3), "unit": "GB/s", "cores": 1,
+                           "kind": "oracle", "sample": "the first eighth of the rows (33,554,432 elements): "
+                           "generation %.2f s, injection %.2f s, check %.2f s" % (tg, ti, tc)}
+    cfg = W.MIXED_STREAM
+    sample = [c for c in cmds if c.nbytes <= 64 * (1 << 20)][:8]
+    total, secs = 0, 0.0
+    for c in sample:
+        dtn = W.DTYPE_NAME[c.dtype]
+        tg, x = t(lambda: oracle.gen(dtn, c.n, c.value_seed, 0, c.dist, c.p0, c.p1))
+        ti, (y, _) = t(lambda: oracle.inject(x, dtn, c.mask_seed, c.rate, cfg["delta"], oracle.INJ_ROUND))
+        tc, _ = t(lambda: oracle.check(y, dtn, x, dtn, c.rtol, c.atol))
+        secs += tg + ti + tc
+        total += c.nbytes * 5
+    secs += flush_s(cfg["flush_bytes"], len(sample), 2)
+    total += len(sample) * cfg["flush_bytes"]
+    out["mixed_stream"] = {"value": round(total / secs / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+                           "sample": "the first %d commands of at most 64 MiB (%s), with one 512 MiB flush each "
+                                     "(2 fills timed, scaled)" % (len(sample), ", ".join(str(c.index) for c in sample))}
+    return out
+
+
+def run_configs(with_cpu=True):
     """The other commands end to end: gemm_tiny (gen + check + 100 reps with a
     512 MiB flush in a region), check_stress (gen + inject + check of 256M
     fp16), mixed_stream (64 derived commands: gen, inject, check with the
@@ -382,6 +437,9 @@ def run_configs():
                                        "wall_GBps": round(total / wall / 1e9, 1),
                                        "commands_per_s": round(len(cmds) / wall, 1)}
     krex.detach()
+    if with_cpu:
+        for k, v in configs_cpu_baseline(cmds).items():
+            out["commands"][k]["cpu_baseline"] = v
     return out
 
 
@@ -427,7 +485,7 @@ def main():
         print(json.dumps(run_kernels()), flush=True)
         return
     if args.configs:
-        print(json.dumps(run_configs()), flush=True)
+        print(json.dumps(run_configs(not args.no_cpu_baseline)), flush=True)
         return
     if args.valu_rates:
         import subprocess
