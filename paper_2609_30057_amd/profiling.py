@@ -179,7 +179,7 @@ def _op_cost(op, rates):
                         ("v_mov", "v_and_b32"), ("v_rcp", "v_rcp_f32"), ("v_sqrt", "v_sqrt_f32"),
                         ("v_mad_u64", "v_mad_u64_u32"), ("v_mul_hi", "v_mul_hi_u32"), ("v_perm", "v_perm_b32")):
         if base.startswith(prefix):
-            return rates[ref]
+            return rates.get(ref, 4.0)
     return 4.0   # unmeasured: the half-rate cost most conversions and 64-bit operations have
 
 

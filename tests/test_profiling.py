@@ -1,0 +1,119 @@
+"""The profile summarisers on synthetic rocprofv3 output: the HBM traffic
+table (copy-calibrated FETCH_SIZE / WRITE_SIZE, and exact read bytes from the
+read-request counters by size) and the vector-issue model of the generation
+kernels (per-unit instruction path of the gfx950 assembly, weighted by issue
+cost, against the launch's waves and duration)."""
+import csv
+import json
+import os
+
+import pytest
+
+from paper_2609_30057_amd import profiling as P
+
+GIB = 1 << 30
+FIELDS = ["Correlation_Id", "Dispatch_Id", "Agent_Id", "Queue_Id", "Process_Id", "Thread_Id", "Grid_Size",
+          "Kernel_Id", "Kernel_Name", "Workgroup_Size", "LDS_Block_Size", "Scratch_Size", "VGPR_Count",
+          "Accum_VGPR_Count", "SGPR_Count", "Counter_Name", "Counter_Value", "Start_Timestamp", "End_Timestamp"]
+
+
+def _counters(path, rows):
+    """rows: (kernel name, counter, value) per dispatch."""
+    os.makedirs(path, exist_ok=True)
+    with open(os.path.join(path, "pmc_counter_collection.csv"), "w", newline="") as f:
+        w = csv.DictWriter(f, FIELDS)
+        w.writeheader()
+        for i, (k, c, v) in enumerate(rows):
+            w.writerow({"Correlation_Id": i, "Dispatch_Id": i, "Agent_Id": "Agent 1", "Queue_Id": 1, "Process_Id": 1,
+                        "Thread_Id": 1, "Grid_Size": 256, "Kernel_Id": 1, "Kernel_Name": k, "Workgroup_Size": 256,
+                        "LDS_Block_Size": 0, "Scratch_Size": 0, "VGPR_Count": 8, "Accum_VGPR_Count": 0,
+                        "SGPR_Count": 16, "Counter_Name": c, "Counter_Value": v, "Start_Timestamp": 0,
+                        "End_Timestamp": 1})
+
+
+RATES = {"v_fma_f32": 2.0, "v_add_f32": 1.9, "v_add_u32": 1.9, "v_and_b32": 1.9, "v_lshrrev_b32": 1.8,
+         "v_bitop3_b32": 1.9, "v_fmaak_f32": 1.9, "v_mul_f32": 1.9, "v_max_f32": 3.6, "v_max3_f32": 3.6,
+         "v_cndmask_b32": 3.6, "v_perm_b32": 3.6, "v_bfe_u32": 3.6, "v_mul_hi_u32": 3.6, "v_mad_u64_u32": 3.7,
+         "v_cvt_f32_u32": 3.6, "v_cvt_f32_f16": 3.6, "v_cvt_f32_fp8": 3.6, "v_cvt_pk_bf16_f32": 3.6,
+         "v_cvt_pk_f16_f32": 3.6, "v_cmp_lt_f32": 3.7, "v_rcp_f32": 7.2, "v_sqrt_f32": 7.2,
+         "v_cvt_pk_fp8_f32": 7.2}
+
+
+class Args:
+    def __init__(self, **kw):
+        self.__dict__.update(kw)
+
+
+def test_traffic_scales_by_the_copy_and_uses_exact_read_bytes(tmp_path):
+    copy = "__amd_rocclr_copyBuffer"
+    check = "void krex::k_check<1, 0, true, 2>(unsigned char const*)"
+    flush = "krex::k_flush(HIP_vector_type<unsigned int, 4u>*, unsigned long, unsigned int)"
+    # FETCH_SIZE counts a 128-byte request as 64 bytes: the 1 GiB copy reads as 512 MiB.
+    _counters(tmp_path / "fetch", [(copy, "FETCH_SIZE", GIB / 2 / 1024), (check, "FETCH_SIZE", 60 * 1024),
+                                   (flush, "FETCH_SIZE", 0.0)])
+    _counters(tmp_path / "write", [(copy, "WRITE_SIZE", GIB / 1024), (check, "WRITE_SIZE", 0.0),
+                                   (flush, "WRITE_SIZE", GIB / 1024)])
+    # the check: 100 MiB in 128-byte requests plus 1 MiB in 64-byte ones
+    _counters(tmp_path / "rdreq", [(copy, "TCC_EA0_RDREQ_32B_sum", 0), (copy, "TCC_EA0_RDREQ_64B_sum", 0),
+                                   (copy, "TCC_EA0_RDREQ_128B_sum", GIB / 128),
+                                   (check, "TCC_EA0_RDREQ_32B_sum", 0), (check, "TCC_EA0_RDREQ_64B_sum", 2**20 / 64),
+                                   (check, "TCC_EA0_RDREQ_128B_sum", 100 * 2**20 / 128),
+                                   (flush, "TCC_EA0_RDREQ_32B_sum", 0), (flush, "TCC_EA0_RDREQ_64B_sum", 0),
+                                   (flush, "TCC_EA0_RDREQ_128B_sum", 0)])
+    out, js = tmp_path / "t.md", tmp_path / "t.json"
+    P.cmd_traffic(Args(fetch=str(tmp_path / "fetch"), write=str(tmp_path / "write"), rdreq=str(tmp_path / "rdreq"),
+                       out=str(out), out_json=str(js), cmd="x", title="t", workload="w",
+                       algo=json.dumps({"krex::k_check<1, 0, true, 2>": 100 * 2**20, "krex::k_flush": GIB})))
+    data = json.load(open(js))
+    assert data["calibration"]["fetch_scale"] == pytest.approx(2.0)
+    assert data["calibration"]["write_scale"] == pytest.approx(1.0)
+    chk = data["k_check/w"]
+    assert chk["fetch_bytes"] == 101 * 2**20          # exact bytes, not 2 x 60 MiB
+    assert chk["hbm_bytes_per_launch"] == 101 * 2**20
+    assert data["k_flush/w"]["hbm_bytes_per_launch"] == GIB
+    text = out.read_text()
+    assert "1024.0 MiB read (1024 expected)" in text
+    assert "| `krex::k_check<1, 0, true, 2>` | 1 | 120.0 | 101.0 | 0.0 | 100.0 | 1.010 |" in text
+
+
+def test_issue_costs_cover_the_hot_instructions():
+    rates = RATES
+    assert P._op_cost("v_mad_u64_u32", rates) == 3.7
+    assert P._op_cost("v_cndmask_b32_e64", rates) == 3.6        # encoding suffix dropped
+    assert P._op_cost("v_fmac_f32_e32", rates) == 2.0            # fmac costs as fma
+    assert P._op_cost("v_cmp_ge_u64_e32", rates) == 3.7          # compares cost as the measured compare
+    assert P._op_cost("v_cvt_pk_fp8_f32", rates) == 7.2
+    assert P._op_cost("v_xor_b32_e32", rates) == 1.9             # bitwise ops as v_and
+    assert P._op_cost("v_sqrt_f32_e64", rates) == 7.2
+    assert P._op_cost("v_unmeasured_op", rates) == 4.0
+
+
+def test_issue_model_of_a_generation_launch(tmp_path):
+    """The unit path of the fp32 uniform kernel (power-of-two range) holds
+    Philox's 32x32->64 multiplies and three-way xors, and the model's time is
+    waves x weighted cycles over 1024 SIMDs x 2.4 GHz."""
+    from paper_2609_30057_amd import build as B
+    asm = open(B.emit_asm(os.path.join(B.BUILD, "kernels_test.s"))).read()
+    ops = P._unit_path(asm, "_ZN4krex5k_genILi0ELi0ELb1EEEvNS_9GenParamsE")
+    assert ops.count("v_mad_u64_u32") >= 18 and ops.count("v_bitop3_b32") >= 18
+    assert any(o.startswith("v_fma") for o in ops)              # the fused uniform transform
+    rates = {"cycles": RATES}
+    rj = tmp_path / "rates.json"
+    rj.write_text(json.dumps(rates))
+    trace = tmp_path / "trace.csv"
+    fields = ["Kind", "Kernel_Name", "Start_Timestamp", "End_Timestamp", "Grid_Size_X"]
+    with open(trace, "w", newline="") as f:
+        w = csv.DictWriter(f, fields)
+        w.writeheader()
+        for _ in range(3):
+            w.writerow({"Kind": "KERNEL_DISPATCH", "Kernel_Name": "void krex::k_gen<0, 0, true>(krex::GenParams)",
+                        "Start_Timestamp": 1000, "End_Timestamp": 41000, "Grid_Size_X": 1 << 24})
+    out = tmp_path / "m.md"
+    P.cmd_valu_model(Args(rates=str(rj), trace=str(trace), out=str(out), cmd="x", title="t", cus=256))
+    row = [l for l in out.read_text().splitlines() if "k_gen<0, 0, true>" in l][0].split("|")
+    cyc = sum(P._op_cost(o, rates["cycles"]) for o in ops)
+    waves = (1 << 24) / 64
+    assert int(row[2]) == len(ops)
+    assert float(row[5]) == pytest.approx(waves * cyc / (1024 * 2.4e9) * 1e6, abs=0.06)
+    assert float(row[6]) == pytest.approx((1 << 24) * 16 / 8e12 * 1e6, abs=0.06)   # HBM time of 16 B per unit
+    assert float(row[8]) == pytest.approx(40.0)
