@@ -17,7 +17,7 @@ the step's 200.2 GiB). The timed-region inflation half of the metric is
 measured by `--fidelity` (Section 6.3, Eq. 1), which prints its own line.
 
 The default run also measures that half briefly after the timed steps
-(`inflation_p95_1ms`: 1 ms probes, 200 single-shot samples in regions, a
+(`inflation_p95_1ms`: 1 ms probes, 1000 single-shot samples in regions, a
 native repeat and 7 gated sibling processes), unless --no-fidelity.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--no-fidelity]
@@ -218,7 +218,7 @@ def run_gemm_large(steps, warmup, with_cpu):
     return out
 
 
-def short_fidelity(samples=200):
+def short_fidelity(samples=1000):
     """The timing-fidelity half of the metric, briefly: P = p95(t / t_native)
     - 1 (Eq. 1) for the 1 ms probe, single-shot inside regions, with 7 sibling
     processes looping the check_stress command off-region through the gate,

@@ -1145,10 +1145,24 @@ hipError_t launch_check(const void *a, int dta, const void *b, int dtb, uint64_t
 // dispatch-ordered shape streams writes at ~85% of HBM peak, well above
 // persistent grid-stride loops (whose 2048 concurrently active blocks spread
 // each wave of stores across the whole buffer).
+//
+// The stores carry the system-scope coherence bits (sc0 sc1): they write
+// through L2 without allocating there, which streams ~2% faster, and still
+// allocate in the Infinity Cache, whose contents the flush exists to evict
+// (a 64 MiB working set re-read after a 1 GiB flush runs at HBM speed, not
+// at Infinity Cache speed). L2 needs no eviction: the runtime writes back and
+// invalidates L2 at kernel boundaries, so a working set read by one launch
+// misses L2 in the next one with or without a flush (measured with the L2
+// hit counters). Non-temporal stores would leave the Infinity Cache intact.
 __global__ __launch_bounds__(kThreads) void k_flush(uint4 *buf, uint64_t nvec, uint32_t pattern)
 {
+    typedef unsigned int v4u __attribute__((ext_vector_type(4)));
     const uint64_t i = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (i < nvec) buf[i] = make_uint4(pattern, pattern, pattern, pattern);
+    if (i < nvec) {
+        uint4 *p = buf + i;
+        const v4u v = {pattern, pattern, pattern, pattern};
+        asm volatile("global_store_dwordx4 %0, %1, off sc0 sc1" ::"v"(p), "v"(v) : "memory");
+    }
 }
 
 hipError_t launch_flush(void *buf, uint64_t bytes, uint32_t pattern, hipStream_t s)
