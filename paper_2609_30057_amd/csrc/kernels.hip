@@ -102,7 +102,7 @@ __global__ __launch_bounds__(kThreads) void k_gen(GenParams P)
         }
         const uint64_t j0 = 4 * bfirst - P.offset;
         if (P.vec && j0 + 4 * G <= P.n) {
-            *reinterpret_cast<uint4 *>(P.dst + j0 * ES) = pk.v;
+            store16_stream(P.dst + j0 * ES, pk.v);
         } else {
 #pragma unroll
             for (int e = 0; e < 4 * G; ++e) {
@@ -322,7 +322,7 @@ __global__ __launch_bounds__(kThreads) void k_gen_packed(PackedParams P)
         }
         const uint64_t q0 = unit * (uint64_t)E;
         if (P.vec && q0 >= P.offset && q0 - P.offset + E <= P.n) {
-            *reinterpret_cast<uint4 *>(P.dst + (q0 - P.offset) * ES) = pk.v;
+            store16_stream(P.dst + (q0 - P.offset) * ES, pk.v);
         } else {
 #pragma unroll
             for (int e = 0; e < E; ++e) {
@@ -433,7 +433,7 @@ __global__ __launch_bounds__(kThreads) void k_xform(XformParams P)
                 }
             }
             if constexpr (DT != U32) pack_narrow<DT, DIST == BITCAST>(v, pk.w);
-            *reinterpret_cast<uint4 *>(P.dst + j0 * ES) = pk.v;
+            store16_stream(P.dst + j0 * ES, pk.v);
         } else {
             for (int e = 0; e < 4 * G; ++e) {
                 const uint64_t j = j0 + (uint64_t)e;
@@ -548,7 +548,7 @@ __global__ __launch_bounds__(kThreads) void k_inject(InjectParams P)
                 uint4 v;
                 T s[4 * G];
             } pk;
-            pk.v = *reinterpret_cast<const uint4 *>(P.x + j0 * ES);
+            pk.v = load16_stream(P.x + j0 * ES);
 #pragma unroll
             for (int i = 0; i < G; ++i) {
                 const words4 w = philox_block(bfirst + i, P.k0, P.k1);
@@ -556,7 +556,7 @@ __global__ __launch_bounds__(kThreads) void k_inject(InjectParams P)
                 for (int l = 0; l < 4; ++l)
                     if ((uint64_t)w.v[l] < P.T) pk.s[4 * i + l] = perturb<DT, MODE>(pk.s[4 * i + l], P.delta);
             }
-            *reinterpret_cast<uint4 *>(P.y + j0 * ES) = pk.v;
+            store16_stream(P.y + j0 * ES, pk.v);
         } else {
             for (int i = 0; i < G; ++i) {
                 const words4 w = philox_block(bfirst + i, P.k0, P.k1);
@@ -742,9 +742,9 @@ struct ChunkIO {
     __device__ __forceinline__ static void load_raw(const uint8_t *a, const uint8_t *b, uint64_t c, Raw &r)
     {
 #pragma unroll
-        for (int i = 0; i < VA; ++i) r.a.v[i] = reinterpret_cast<const uint4 *>(a)[c * VA + i];
+        for (int i = 0; i < VA; ++i) r.a.v[i] = load16_stream(a + (c * VA + i) * 16);
 #pragma unroll
-        for (int i = 0; i < VB; ++i) r.b.v[i] = reinterpret_cast<const uint4 *>(b)[c * VB + i];
+        for (int i = 0; i < VB; ++i) r.b.v[i] = load16_stream(b + (c * VB + i) * 16);
     }
 
     // fp8 elements are converted two at a time straight from their 32-bit
@@ -1146,8 +1146,9 @@ hipError_t launch_check(const void *a, int dta, const void *b, int dtb, uint64_t
 // persistent grid-stride loops (whose 2048 concurrently active blocks spread
 // each wave of stores across the whole buffer).
 //
-// The stores carry the system-scope coherence bits (sc0 sc1): they write
-// through L2 without allocating there, which streams ~2% faster, and still
+// The stores (store16_stream) carry the system-scope coherence bits
+// (sc0 sc1): they write through L2 without allocating there, which streams
+// ~2% faster, and still
 // allocate in the Infinity Cache, whose contents the flush exists to evict
 // (a 64 MiB working set re-read after a 1 GiB flush runs at HBM speed, not
 // at Infinity Cache speed). L2 needs no eviction: the runtime writes back and
@@ -1156,13 +1157,8 @@ hipError_t launch_check(const void *a, int dta, const void *b, int dtb, uint64_t
 // hit counters). Non-temporal stores would leave the Infinity Cache intact.
 __global__ __launch_bounds__(kThreads) void k_flush(uint4 *buf, uint64_t nvec, uint32_t pattern)
 {
-    typedef unsigned int v4u __attribute__((ext_vector_type(4)));
     const uint64_t i = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (i < nvec) {
-        uint4 *p = buf + i;
-        const v4u v = {pattern, pattern, pattern, pattern};
-        asm volatile("global_store_dwordx4 %0, %1, off sc0 sc1" ::"v"(p), "v"(v) : "memory");
-    }
+    if (i < nvec) store16_stream(buf + i, make_uint4(pattern, pattern, pattern, pattern));
 }
 
 hipError_t launch_flush(void *buf, uint64_t bytes, uint32_t pattern, hipStream_t s)

@@ -48,7 +48,7 @@ def kernel_source_sha(kernel):
     parts = re.split(r"^// -{10,} (.+?)\s*$", text, flags=re.M)
     sections = {parts[i].strip(): parts[i + 1] for i in range(1, len(parts) - 1, 2)}
     body = sections[SECTION_OF[kernel]]
-    if kernel not in ("k_flush", "k_probe", "k_sgemm"):
+    if kernel not in ("k_probe", "k_sgemm"):
         body += open(DEVICE_HPP).read()
     return hashlib.sha256(body.encode()).hexdigest()
 
