@@ -1100,12 +1100,16 @@ static hipError_t check_ab_d(const void *a, const void *b, uint64_t n, float rto
     return launch(k_check_final, dim3(1), dim3(kFinalThreads), s, (const CheckPartial *)parts, (uint32_t)G, n, out);
 }
 
-// Depth of the load ring: fp8 pairs evaluate 16 elements per 32 bytes
-// loaded, twice the work per byte of the other pairs, and need a third
-// buffer in flight to keep HBM busy (measured on gfx950: fp8 x fp8 +12%; no
-// gain for the other pairs, whose extra registers only lower occupancy).
+// Depth of the load ring: a third buffer in flight pays for pairs of one-
+// and two-byte operands (one 16-byte vector of each per chunk; measured on
+// gfx950 with non-temporal loads: fp16 x fp16 -5%, fp8 x fp8 -13%), not for
+// pairs with a four-byte operand, whose extra registers only lower
+// occupancy.
 template <int DA, int DB>
-static constexpr int check_depth() { return (DA == F8 && DB == F8) ? 3 : 2; }
+static constexpr int check_depth()
+{
+    return (dtype_traits<DA>::size == dtype_traits<DB>::size && dtype_traits<DA>::size <= 2) ? 3 : 2;
+}
 
 template <int DA, int DB>
 static hipError_t check_ab(const void *a, const void *b, uint64_t n, float rtol, float atol, void *scratch,
