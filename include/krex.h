@@ -183,10 +183,13 @@ krex_status krex_check(const void *a, int32_t dta, const void *b, int32_t dtb, u
 
 /* --- cache flush ------------------------------------------------------------
  * Writes `pattern` to every 32-bit word of buf[0..bytes) (device, 16-byte
- * aligned, bytes a multiple of 16) with ordinary allocating stores, evicting
- * earlier contents of the L2 and Infinity Cache when bytes exceeds their
- * size (Section 2.1: flush between timed iterations; Section 4.2 step 5:
- * memset over a cache-sized buffer). */
+ * aligned, bytes a multiple of 16) with stores that allocate in the
+ * Infinity Cache (written through L2 with system-scope coherence), evicting
+ * its earlier contents when bytes exceeds its 256 MB (Section 2.1: flush
+ * between timed iterations; Section 4.2 step 5: memset over a cache-sized
+ * buffer). L2 holds nothing across kernel launches on gfx950 (the runtime
+ * writes it back and invalidates it at kernel boundaries), so the Infinity
+ * Cache is the cache a timed launch could otherwise inherit data from. */
 krex_status krex_flush(void *buf, uint64_t bytes, uint32_t pattern, void *stream);
 
 /* --- probe kernel -----------------------------------------------------------
