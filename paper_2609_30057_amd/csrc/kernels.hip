@@ -685,12 +685,16 @@ __device__ __forceinline__ void ratio_update(float A, float B, LaneAcc &acc)
 // or their difference overflows, and is then never close; clamping the
 // threshold to the largest float excludes it in the same comparison (a NaN
 // threshold, 0 x inf, arises only with |b| = inf, where d0 is inf or NaN and
-// the verdict is a mismatch either way).
+// the verdict is a mismatch either way). CLAMP = false when neither operand
+// type has an infinity and their difference cannot overflow (fp8 e4m3fn
+// pairs: |a|, |b| <= 448): d0 is then never +inf and the threshold never
+// NaN, so the clamp cannot change a verdict.
+template <bool CLAMP = true>
 __device__ __forceinline__ uint64_t count_elem(float A, float B, float d0, float ab, float rtol, float atol,
                                                LaneAcc &acc)
 {
     const float rt = rtol * ab;
-    const float thr = __builtin_fminf(atol + rt, 0x1.fffffep127f);
+    const float thr = CLAMP ? __builtin_fminf(atol + rt, 0x1.fffffep127f) : atol + rt;
     const uint64_t ne = __ballot(A != B);
     const uint64_t far = __ballot(!(d0 <= thr));
     const uint64_t unord = __ballot(__builtin_isunordered(A, B));
@@ -847,7 +851,7 @@ __global__ __launch_bounds__(kThreads) void k_check(const uint8_t *a, const uint
         for (int e = 0; e < E; ++e) {
             const float d0 = __builtin_fabsf(A[e] - B[e]);
             const float ab = __builtin_fabsf(B[e]);
-            const uint64_t differ = count_elem(A[e], B[e], d0, ab, rtol, atol, acc);
+            const uint64_t differ = count_elem<!(DA == F8 && DB == F8)>(A[e], B[e], d0, ab, rtol, atol, acc);
             // Equal operands (ratio 0, or 0/0) and unordered ones (NaN d)
             // never raise the maximum: only ordered, differing elements are
             // candidates (otherwise every zero reference would be one).

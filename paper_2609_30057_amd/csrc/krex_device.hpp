@@ -313,14 +313,13 @@ __device__ __forceinline__ float sqrt_nonneg_normal(float t)
 // 16-bit head of ln 2.
 __device__ __forceinline__ float ln_f32(float x)
 {
-    const uint32_t ix = __float_as_uint(x);
-    int32_t e = (int32_t)(ix >> 23) - 127;
-    const uint32_t mb = ix & 0x7FFFFFu;
-    float m = __uint_as_float(mb | 0x3F800000u);
-    if (mb > 0x3504F3u) {
-        m = m * 0.5f;
-        e = e + 1;
-    }
+    // The split without a compare: adding 0x4AFB0C to the bits of x carries
+    // into the exponent exactly when the mantissa field exceeds 0x3504F3
+    // (that of fp32(sqrt 2)); the low 23 bits plus the bits of
+    // fp32(sqrt(1/2)) + 1 ulp, 0x3F3504F4, then give 1.mb or 0.5 x 1.mb.
+    const uint32_t iy = __float_as_uint(x) + 0x004AFB0Cu;
+    const int32_t e = (int32_t)(iy >> 23) - 127;
+    const float m = __uint_as_float((iy & 0x7FFFFFu) + 0x3F3504F4u);
     const float f = m - 1.0f;
     const float den = 2.0f + f;
     const float s = div_on_ln_domain(f, den);
