@@ -222,13 +222,17 @@ def short_fidelity(samples=1000):
     """The timing-fidelity half of the metric, briefly: P = p95(t / t_native)
     - 1 (Eq. 1) for the 1 ms probe, single-shot inside regions, with 7 sibling
     processes looping the check_stress command off-region through the gate,
-    next to a native repeat. The full sweep is --fidelity."""
+    next to a native repeat (P of a second run alone: the spread of
+    single-shot timings, the noise floor) and the median-of-10 variant
+    (Section 6.6). The full sweep is --fidelity."""
     from paper_2609_30057_amd import fidelity
     try:
         r = fidelity.run(samples=samples, durations_ms=(1.0,), modes=("control", "gated"))
     except Exception as e:   # the throughput line stays valid without it
         return {"value": None, "error": "%s: %s" % (type(e).__name__, e)}
     return {"value": r["P"]["1.0"]["gated"], "unit": "%", "native_repeat": r["P"]["1.0"]["control"],
+            "median_of_10": r["P_median_of_10"]["1.0"]["gated"],
+            "median_of_10_native_repeat": r["P_median_of_10"]["1.0"]["control"],
             "probe_ms": 1.0, "samples": samples, "siblings": r["siblings"],
             "sibling_GBps": r["sibling_GBps"].get("gated"), "drain_ms_p95": r["drain_ms"]["gated"]["p95"],
             "target": "<= 1%"}

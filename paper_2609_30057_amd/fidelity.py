@@ -7,6 +7,9 @@ kernel duration, 0.1 / 1 / 10 ms); Section 6.5 (ungated sharing as the
 unprotected baseline); Section 6.6 (single-shot and median-of-ten timing).
 
 Procedure, on one GPU:
+  0. settle: probe launches back to back for about 2 s, so the device's
+     clock and thermal state after earlier work (a benchmark just before)
+     does not drift between the native run and the later ones;
   1. calibrate the probe's iteration count to each target duration, alone;
   2. native: `samples` single-shot timings per duration, alone (each sample:
      region entry, warm-up launches for about 3 ms (or exactly one with
@@ -105,6 +108,16 @@ def _torch_siblings(k, shm, stop_path):
     return procs
 
 
+def _settle(krex, sink, seconds):
+    """Back-to-back probe launches for about `seconds`, untimed."""
+    import torch
+    t0 = time.perf_counter()
+    fn = krex.probe_launcher(20000, sink)
+    while time.perf_counter() - t0 < seconds:
+        krex.time_loop(fn, 0, 20)
+    torch.cuda.synchronize()
+
+
 def _calibrate(krex, sink, target_ms):
     iters = 20000
     for _ in range(4):
@@ -131,7 +144,8 @@ def _measure(krex, plan, samples, fl, sink, gap_ms, warmup_ms=0.0):
     return times, drains
 
 
-def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, modes=None, warmup_ms=None):
+def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, modes=None, warmup_ms=None,
+        settle_s=2.0):
     import torch
 
     import paper_2609_30057_amd as krex
@@ -163,6 +177,7 @@ def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, mode
             os.environ.pop("KREX_REGION_CPU", None)
         krex.attach(0, shm_name=shm, gated=gated, cpu_exclusive=frozen)
         if mode == "native":
+            _settle(krex, sink, settle_s)
             plan = []
             for d in durations_ms:
                 iters, t = _calibrate(krex, sink, d)

@@ -42,13 +42,20 @@ SECTION_OF = {"k_flush": "flush", "k_check": "check", "k_check_final": "check", 
               "k_inject": "injection", "k_xform": "words transform", "k_probe": "probe", "k_sgemm": "fixture"}
 
 
-def kernel_source_sha(kernel):
-    """sha256 of the source that defines `kernel` (short name, e.g. k_flush)."""
-    text = open(KERNELS_HIP).read()
+def _sections(path):
+    text = open(path).read()
     parts = re.split(r"^// -{10,} (.+?)\s*$", text, flags=re.M)
-    sections = {parts[i].strip(): parts[i + 1] for i in range(1, len(parts) - 1, 2)}
-    body = sections[SECTION_OF[kernel]]
-    if kernel not in ("k_probe", "k_sgemm"):
+    return {parts[i].strip(): parts[i + 1] for i in range(1, len(parts) - 1, 2)}
+
+
+def kernel_source_sha(kernel):
+    """sha256 of the source that defines `kernel` (short name, e.g. k_flush):
+    its section of kernels.hip plus what it uses of the device header (the
+    flush only its streaming stores, the others the whole header)."""
+    body = _sections(KERNELS_HIP)[SECTION_OF[kernel]]
+    if kernel == "k_flush":
+        body += _sections(DEVICE_HPP)["streaming memory"]
+    elif kernel not in ("k_probe", "k_sgemm"):
         body += open(DEVICE_HPP).read()
     return hashlib.sha256(body.encode()).hexdigest()
 
