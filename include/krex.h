@@ -167,6 +167,19 @@ krex_status krex_transform_words(void *dst, int32_t dtype, uint64_t n, const uin
 krex_status krex_inject(void *y, const void *x, int32_t dtype, uint64_t n, uint64_t mask_seed,
                         uint64_t mask_offset, double rate, float delta, int32_t mode, void *stream);
 
+/* Generation and injection in one call: x = krex_gen(x, dtype, n, seed,
+ * offset, dist, p0, p1) and y = krex_inject(y, x, dtype, n, mask_seed,
+ * mask_offset, rate, delta, mode), with the same results bit for bit. A
+ * benchmarking command's input and the perturbed output that stands in for
+ * a wrong candidate (Section 2.1) come from one pass that writes x and y
+ * without reading x back when offset and mask_offset are multiples of 4 and
+ * x, y are 16-byte aligned (otherwise the two kernels run in order). x and y
+ * (device, aligned to the element size) must not overlap. Arguments and
+ * errors as for the two calls; dtype not KREX_U32. */
+krex_status krex_gen_inject(void *x, void *y, int32_t dtype, uint64_t n, uint64_t seed, uint64_t offset,
+                            int32_t dist, float p0, float p1, uint64_t mask_seed, uint64_t mask_offset, double rate,
+                            float delta, int32_t mode, void *stream);
+
 /* --- correctness check ----------------------------------------------------
  * Compares a (candidate, dtype dta) with b (reference, dtype dtb), n elements
  * each, device memory, and writes *out (device-accessible; overwritten, no

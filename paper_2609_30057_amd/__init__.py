@@ -110,6 +110,7 @@ def lib():
             "krex_gen_packed": (i32, [vp, i32, u64, u64, u64, i32, f32, f32, vp]),
             "krex_transform_words": (i32, [vp, i32, u64, vp, i32, f32, f32, vp]),
             "krex_inject": (i32, [vp, vp, i32, u64, u64, u64, f64, f32, i32, vp]),
+            "krex_gen_inject": (i32, [vp, vp, i32, u64, u64, u64, i32, f32, f32, u64, u64, f64, f32, i32, vp]),
             "krex_check": (i32, [vp, i32, vp, i32, u64, f32, f32, vp, vp]),
             "krex_flush": (i32, [vp, u64, u32, vp]),
             "krex_probe": (i32, [u64, vp, vp]),
@@ -228,6 +229,25 @@ def inject(y, x, mask_seed, rate, delta, mode="exact", mask_offset=0, stream=Non
     _chk(lib().krex_inject(_dev(y), _dev(x), dtype_code(x.dtype), x.numel(), mask_seed & (2**64 - 1),
                            mask_offset, float(rate), float(delta), m, _stream(stream)), "krex_inject")
     return y
+
+
+def gen_inject(x, y, seed, offset=0, dist="uniform", p0=None, p1=None, mask_seed=0, rate=0.0, delta=0.0,
+               mode="exact", mask_offset=0, stream=None):
+    """x = gen(x, seed, offset, dist, p0, p1) and y = inject(y, x, mask_seed,
+    rate, delta, mode, mask_offset) in one call (one pass when both offsets
+    are multiples of 4)."""
+    if y.dtype != x.dtype or y.numel() != x.numel():
+        raise ValueError("x and y must have the same dtype and size")
+    d = _dist(dist)
+    if p0 is None:
+        p0 = -1.0 if d == UNIFORM else 0.0
+    if p1 is None:
+        p1 = 1.0 if d == UNIFORM else (1.0 if d == NORMAL else 0.0)
+    m = _MODES[mode] if isinstance(mode, str) else int(mode)
+    _chk(lib().krex_gen_inject(_dev(x), _dev(y), dtype_code(x.dtype), x.numel(), seed & (2**64 - 1), offset, d, p0,
+                               p1, mask_seed & (2**64 - 1), mask_offset, float(rate), float(delta), m,
+                               _stream(stream)), "krex_gen_inject")
+    return x, y
 
 
 def check_result_buffer(device=None):

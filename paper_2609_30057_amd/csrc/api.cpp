@@ -388,6 +388,31 @@ krex_status krex_inject(void *y, const void *x, int32_t dtype, uint64_t n, uint6
     return submit(s, [&] { return krex::launch_inject(y, x, dtype, n, mask_seed, mask_offset, T, delta, mode, s); });
 }
 
+krex_status krex_gen_inject(void *x, void *y, int32_t dtype, uint64_t n, uint64_t seed, uint64_t offset,
+                            int32_t dist, float p0, float p1, uint64_t mask_seed, uint64_t mask_offset, double rate,
+                            float delta, int32_t mode, void *stream)
+{
+    const size_t es = elem_size(dtype);
+    if (es == 0 || dtype == KREX_U32) return KREX_EINVAL;
+    if (!gen_params_ok(dist, p0, p1)) return KREX_EINVAL;
+    if (!(rate >= 0.0 && rate <= 1.0)) return KREX_EINVAL;
+    if (!finite_f(delta)) return KREX_EINVAL;
+    if (mode != KREX_INJ_ROUND && mode != KREX_INJ_EXACT) return KREX_EINVAL;
+    if (n > 0 && (offset > UINT64_MAX - (n - 1) || mask_offset > UINT64_MAX - (n - 1))) return KREX_EINVAL;
+    if (n > 0 && (!x || !y)) return KREX_EINVAL;
+    if (!aligned(x, es) || !aligned(y, es)) return KREX_EALIGN;
+    if (n == 0) return KREX_OK;
+    const uintptr_t xa = (uintptr_t)x, ya = (uintptr_t)y, len = (uintptr_t)(n * es);
+    if (xa < ya + len && ya < xa + len) return KREX_EINVAL;   // two outputs: no overlap at all
+    double t = floor(rate * 4294967296.0);
+    const uint64_t T = t <= 0.0 ? 0ull : (t >= 4294967296.0 ? (1ull << 32) : (uint64_t)t);
+    hipStream_t s = (hipStream_t)stream;
+    return submit(s, [&] {
+        return krex::launch_gen_inject(x, y, dtype, n, seed, offset, dist, p0, p1, mask_seed, mask_offset, T, delta,
+                                       mode, s);
+    });
+}
+
 krex_status krex_check(const void *a, int32_t dta, const void *b, int32_t dtb, uint64_t n, float rtol, float atol,
                        krex_check_result *out, void *stream)
 {

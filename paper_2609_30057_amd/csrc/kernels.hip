@@ -102,7 +102,11 @@ __global__ __launch_bounds__(kThreads) void k_gen(GenParams P)
         }
         const uint64_t j0 = 4 * bfirst - P.offset;
         if (P.vec && j0 + 4 * G <= P.n) {
-            store16_stream(P.dst + j0 * ES, pk.v);
+            // vec: offset % 4 == 0; the block's first group starts at element
+            // jb (uniform across the block) and lane t's 16 bytes at jb + 4 G t
+            const uint64_t gb = ((uint64_t)blockIdx.x * P.U + u) * kThreads;
+            const uint64_t jb = 4 * (P.b0 + gb * G) - P.offset;
+            store16_stream(P.dst + jb * ES, 16u * threadIdx.x, pk.v);
         } else {
 #pragma unroll
             for (int e = 0; e < 4 * G; ++e) {
@@ -177,10 +181,11 @@ static hipError_t gen_dt(const GenParams &P, int dist, hipStream_t s)
     }
 }
 
-hipError_t launch_gen(void *dst, int dt, uint64_t n, uint64_t seed, uint64_t offset, int dist, float p0,
-                      float p1, hipStream_t s)
+// Generation parameters of krex_gen (n > 0): Philox key, first block,
+// groups of G blocks, the uniform transform's constants.
+static GenParams make_gen_params(void *dst, int dt, uint64_t n, uint64_t seed, uint64_t offset, int dist, float p0,
+                                 float p1)
 {
-    if (n == 0) return hipSuccess;
     GenParams P;
     P.dst = (uint8_t *)dst;
     P.n = n;
@@ -201,6 +206,15 @@ hipError_t launch_gen(void *dst, int dt, uint64_t n, uint64_t seed, uint64_t off
     }
     P.ngroups = (nblocks + (uint64_t)G - 1) / (uint64_t)G;
     P.vec = ((offset & 3u) == 0 && ((uintptr_t)dst & 15u) == 0) ? 1 : 0;
+    P.U = 1;
+    return P;
+}
+
+hipError_t launch_gen(void *dst, int dt, uint64_t n, uint64_t seed, uint64_t offset, int dist, float p0,
+                      float p1, hipStream_t s)
+{
+    if (n == 0) return hipSuccess;
+    const GenParams P = make_gen_params(dst, dt, n, seed, offset, dist, p0, p1);
     switch (dt) {
     case F32: return gen_dt<F32>(P, dist, s);
     case BF16: return gen_dt<BF16>(P, dist, s);
@@ -322,7 +336,9 @@ __global__ __launch_bounds__(kThreads) void k_gen_packed(PackedParams P)
         }
         const uint64_t q0 = unit * (uint64_t)E;
         if (P.vec && q0 >= P.offset && q0 - P.offset + E <= P.n) {
-            store16_stream(P.dst + (q0 - P.offset) * ES, pk.v);
+            const uint64_t gb = ((uint64_t)blockIdx.x * P.U + u) * kThreads;
+            const uint64_t qb = (P.u0 + gb) * (uint64_t)E - P.offset;
+            store16_stream(P.dst + qb * ES, 16u * threadIdx.x, pk.v);
         } else {
 #pragma unroll
             for (int e = 0; e < E; ++e) {
@@ -433,7 +449,8 @@ __global__ __launch_bounds__(kThreads) void k_xform(XformParams P)
                 }
             }
             if constexpr (DT != U32) pack_narrow<DT, DIST == BITCAST>(v, pk.w);
-            store16_stream(P.dst + j0 * ES, pk.v);
+            const uint64_t jb = ((uint64_t)blockIdx.x * P.U + u) * kThreads * 4 * G;
+            store16_stream(P.dst + jb * ES, 16u * threadIdx.x, pk.v);
         } else {
             for (int e = 0; e < 4 * G; ++e) {
                 const uint64_t j = j0 + (uint64_t)e;
@@ -556,7 +573,9 @@ __global__ __launch_bounds__(kThreads) void k_inject(InjectParams P)
                 for (int l = 0; l < 4; ++l)
                     if ((uint64_t)w.v[l] < P.T) pk.s[4 * i + l] = perturb<DT, MODE>(pk.s[4 * i + l], P.delta);
             }
-            store16_stream(P.y + j0 * ES, pk.v);
+            const uint64_t gb = ((uint64_t)blockIdx.x * P.U + u) * kThreads;
+            const uint64_t jb = 4 * (P.b0 + gb * G) - P.moff;
+            store16_stream(P.y + jb * ES, 16u * threadIdx.x, pk.v);
         } else {
             for (int i = 0; i < G; ++i) {
                 const words4 w = philox_block(bfirst + i, P.k0, P.k1);
@@ -607,6 +626,118 @@ hipError_t launch_inject(void *y, const void *x, int dt, uint64_t n, uint64_t ms
     case BF16: return inject_dt<BF16>(P, mode, s);
     case F16: return inject_dt<F16>(P, mode, s);
     default: return inject_dt<F8>(P, mode, s);
+    }
+}
+
+// ---------------------------------------------------- generation with injection
+//
+// A command's input and its perturbed copy in one pass: x = krex_gen and
+// y = krex_inject(x), without writing x and reading it back. With the value
+// offset and the mask offset both multiples of 4, element j's value word and
+// mask word are the same lane of their Philox blocks, so a thread unit is
+// G value blocks (one 16-byte vector of x), the G mask blocks of the same
+// elements, and one 16-byte vector of y. The host runs the two separate
+// kernels otherwise.
+
+struct GenInjectParams {
+    GenParams g;       // generation of x (offset % 4 == 0)
+    uint8_t *y;
+    uint32_t m0, m1;   // mask key
+    uint64_t mb0;      // first mask block: mask offset / 4
+    uint64_t T;        // threshold in [0, 2^32]
+    float delta;
+};
+
+template <int DT, int DIST, bool POW2, int MODE>
+__global__ __launch_bounds__(kThreads) void k_gen_inject(GenInjectParams Q)
+{
+    using T = typename dtype_traits<DT>::storage;
+    constexpr int ES = dtype_traits<DT>::size;
+    constexpr int G = group_of<DT>::G;
+    const GenParams &P = Q.g;
+    for (uint32_t u = 0; u < P.U; ++u) {
+        const uint64_t g = ((uint64_t)blockIdx.x * P.U + u) * kThreads + threadIdx.x;
+        if (g >= P.ngroups) break;
+        const uint64_t bfirst = P.b0 + g * G;
+        const uint64_t mfirst = Q.mb0 + g * G;
+        union {
+            uint4 v;
+            uint32_t w[4];
+            T s[4 * G];
+        } px, py;
+        float v[4 * G];
+#pragma unroll
+        for (int i = 0; i < G; ++i)
+            transform4<DIST, POW2>(philox_block(bfirst + i, P.k0, P.k1), P.p0, POW2 ? P.c : P.p1, v + 4 * i);
+        pack_narrow<DT, DIST == BITCAST>(v, px.w);
+        py.v = px.v;
+#pragma unroll
+        for (int i = 0; i < G; ++i) {
+            const words4 m = philox_block(mfirst + i, Q.m0, Q.m1);
+#pragma unroll
+            for (int l = 0; l < 4; ++l)
+                if ((uint64_t)m.v[l] < Q.T) py.s[4 * i + l] = perturb<DT, MODE>(py.s[4 * i + l], Q.delta);
+        }
+        const uint64_t j0 = 4 * bfirst - P.offset;
+        if (P.vec && j0 + 4 * G <= P.n) {
+            const uint64_t gb = ((uint64_t)blockIdx.x * P.U + u) * kThreads;
+            const uint64_t jb = 4 * (P.b0 + gb * G) - P.offset;
+            store16_stream(P.dst + jb * ES, 16u * threadIdx.x, px.v);
+            store16_stream(Q.y + jb * ES, 16u * threadIdx.x, py.v);
+        } else {
+            for (int e = 0; e < 4 * G; ++e) {
+                const uint64_t j = j0 + (uint64_t)e;
+                if (j >= P.n) break;
+                reinterpret_cast<T *>(P.dst)[j] = px.s[e];
+                reinterpret_cast<T *>(Q.y)[j] = py.s[e];
+            }
+        }
+    }
+}
+
+template <int DT, int DIST, bool POW2>
+static hipError_t gen_inject_mode(GenInjectParams Q, int mode, hipStream_t s)
+{
+    uint32_t grid;
+    shape(Q.g.ngroups, 1, &Q.g.U, &grid);
+    if (mode == INJ_ROUND) return launch(k_gen_inject<DT, DIST, POW2, INJ_ROUND>, dim3(grid), dim3(kThreads), s, Q);
+    return launch(k_gen_inject<DT, DIST, POW2, INJ_EXACT>, dim3(grid), dim3(kThreads), s, Q);
+}
+
+template <int DT>
+static hipError_t gen_inject_dt(const GenInjectParams &Q, int dist, int mode, hipStream_t s)
+{
+    switch (dist) {
+    case UNIFORM:
+        return Q.g.pow2 ? gen_inject_mode<DT, UNIFORM, true>(Q, mode, s) : gen_inject_mode<DT, UNIFORM, false>(Q, mode, s);
+    case NORMAL: return gen_inject_mode<DT, NORMAL, false>(Q, mode, s);
+    default: return gen_inject_mode<DT, BITCAST, false>(Q, mode, s);
+    }
+}
+
+hipError_t launch_gen_inject(void *x, void *y, int dt, uint64_t n, uint64_t seed, uint64_t offset, int dist, float p0,
+                             float p1, uint64_t mseed, uint64_t moff, uint64_t T, float delta, int mode,
+                             hipStream_t s)
+{
+    if (n == 0) return hipSuccess;
+    if ((offset & 3u) != 0 || (moff & 3u) != 0 || ((uintptr_t)x & 15u) != 0 || ((uintptr_t)y & 15u) != 0) {
+        const hipError_t e = launch_gen(x, dt, n, seed, offset, dist, p0, p1, s);
+        if (e != hipSuccess) return e;
+        return launch_inject(y, x, dt, n, mseed, moff, T, delta, mode, s);
+    }
+    GenInjectParams Q;
+    Q.g = make_gen_params(x, dt, n, seed, offset, dist, p0, p1);
+    Q.y = (uint8_t *)y;
+    Q.m0 = (uint32_t)mseed;
+    Q.m1 = (uint32_t)(mseed >> 32);
+    Q.mb0 = moff >> 2;
+    Q.T = T;
+    Q.delta = delta;
+    switch (dt) {
+    case F32: return gen_inject_dt<F32>(Q, dist, mode, s);
+    case BF16: return gen_inject_dt<BF16>(Q, dist, mode, s);
+    case F16: return gen_inject_dt<F16>(Q, dist, mode, s);
+    default: return gen_inject_dt<F8>(Q, dist, mode, s);
     }
 }
 
@@ -1154,9 +1285,9 @@ hipError_t launch_check(const void *a, int dta, const void *b, int dtb, uint64_t
 // persistent grid-stride loops (whose 2048 concurrently active blocks spread
 // each wave of stores across the whole buffer).
 //
-// The stores (store16_stream) carry the system-scope coherence bits
-// (sc0 sc1): they write through L2 without allocating there, which streams
-// ~2% faster, and still
+// The stores (store16_stream, raw buffer stores) carry the system-scope
+// coherence bits (sc0 sc1): they write through L2 without allocating there,
+// which streams ~2% faster, and still
 // allocate in the Infinity Cache, whose contents the flush exists to evict
 // (a 64 MiB working set re-read after a 1 GiB flush runs at HBM speed, not
 // at Infinity Cache speed). L2 needs no eviction: the runtime writes back and
@@ -1166,7 +1297,8 @@ hipError_t launch_check(const void *a, int dta, const void *b, int dtb, uint64_t
 __global__ __launch_bounds__(kThreads) void k_flush(uint4 *buf, uint64_t nvec, uint32_t pattern)
 {
     const uint64_t i = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (i < nvec) store16_stream(buf + i, make_uint4(pattern, pattern, pattern, pattern));
+    if (i < nvec) store16_stream(buf + (uint64_t)blockIdx.x * kThreads, 16u * threadIdx.x,
+                                 make_uint4(pattern, pattern, pattern, pattern));
 }
 
 hipError_t launch_flush(void *buf, uint64_t bytes, uint32_t pattern, hipStream_t s)

@@ -81,18 +81,22 @@ __device__ __forceinline__ uint4 load16_stream(const void *p)
     return make_uint4(v.x, v.y, v.z, v.w);
 }
 
-// 16-byte store of a generated output with the system-scope coherence bits:
-// written through L2 without allocating there (L2 does not carry data from
-// one launch to the next on this GPU anyway) and allocated in the Infinity
-// Cache like an ordinary store, ~2% faster for streamed writes. The s_nop
-// is the wait state a store of more than 8 bytes needs before a vector
-// instruction may overwrite its data registers: the compiler inserts it for
-// its own stores but cannot see this one.
-__device__ __forceinline__ void store16_stream(void *p, const uint4 &u)
+// 16-byte store of a generated output with the system-scope coherence bits
+// (sc0 sc1): written through L2 without allocating there (L2 does not carry
+// data from one launch to the next on this GPU anyway) and allocated in the
+// Infinity Cache like an ordinary store, ~2% faster for streamed writes. It
+// is a raw buffer store, so the compiler sees it and keeps the wait states a
+// store needs before its data registers are overwritten. `base` must be the
+// same for every lane of the wave (a block's first byte); `off` is the
+// lane's byte offset from it, below 2^31.
+__device__ __forceinline__ void store16_stream(void *base, uint32_t off, const uint4 &u)
 {
     typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+    constexpr int kSc0Sc1 = 1 | 16;            // cache-policy bits: sc0, sc1
+    constexpr int kRawDword3 = 0x00020000;     // raw buffer: 32-bit data format, no swizzle
+    const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(base, (short)0, 0x7FFFFFFF, kRawDword3);
     const v4u v = {u.x, u.y, u.z, u.w};
-    asm volatile("global_store_dwordx4 %0, %1, off sc0 sc1\n\ts_nop 0" ::"v"(p), "v"(v) : "memory");
+    __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)off, 0, kSc0Sc1);
 }
 
 // ---------------------------------------------------------------- narrowing

@@ -23,6 +23,11 @@ hipError_t launch_xform(void *dst, int dt, uint64_t n, const uint32_t *words, in
                         hipStream_t s);
 hipError_t launch_inject(void *y, const void *x, int dt, uint64_t n, uint64_t mseed, uint64_t moff, uint64_t T,
                          float delta, int mode, hipStream_t s);
+// launch_gen into x, then launch_inject from x into y, as one fused kernel
+// when both offsets are multiples of 4 and x, y are 16-byte aligned.
+hipError_t launch_gen_inject(void *x, void *y, int dt, uint64_t n, uint64_t seed, uint64_t offset, int dist, float p0,
+                             float p1, uint64_t mseed, uint64_t moff, uint64_t T, float delta, int mode,
+                             hipStream_t s);
 // The check reduces per-block partials held in `scratch` (device memory of
 // check_scratch_bytes()); calls that may overlap need distinct scratch.
 size_t check_scratch_bytes();
