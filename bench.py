@@ -291,6 +291,8 @@ def run_kernels():
     rec("gen packed f8 uniform 268M", t_ms(lambda: krex.gen_packed(x8, 5, 0, "uniform", -4.0, 4.0)), x8.numel())
     rec("gen packed f8 normal 268M", t_ms(lambda: krex.gen_packed(x8, 5, 0, "normal")), x8.numel())
     rec("inject f16 exact 268M", t_ms(lambda: krex.inject(y16, x16, 3, 0.001, 0.5)), x16.numel() * 4)
+    rec("gen+inject fused f16 268M", t_ms(lambda: krex.gen_inject(x16, y16, 2, 0, "uniform", -4.0, 4.0, mask_seed=3,
+                                                                   rate=0.001, delta=0.5)), x16.numel() * 4)
     krex.inject(y8, x8, 6, 0.01, 0.25, "round")
     krex.inject(yf, xf, 8, 0.01, 0.5)
     rec("check bf16xf32 16.8M", t_ms(lambda: krex.check(a_bf, b_f32, 1.6e-2, 1e-2, out=out, sync=False)), N * 6)
@@ -426,7 +428,25 @@ def run_configs(with_cpu=True):
         v = krex.decode_check_result(res)
     tg, ti, tc = e0.elapsed_time(e1), e1.elapsed_time(e2), e2.elapsed_time(e3)
     nbytes = m * 2 + m * 4 + m * 4
+    # the same command with generation and injection fused (x and y written
+    # in one pass, x not read back): 8 bytes per element instead of 10
+    for _ in range(2):
+        f0 = ev()
+        krex.gen_inject(x, y, cfg["seed"], 0, "uniform", cfg["p0"], cfg["p1"], mask_seed=cfg["mask_seed"],
+                        rate=cfg["rate"], delta=cfg["delta"], mode="exact")
+        f1 = ev()
+        krex.check(y, x, cfg["rtol"], cfg["atol"], out=res, sync=False)
+        f2 = ev()
+        vf = krex.decode_check_result(res)
+    tf, tcf = f0.elapsed_time(f1), f1.elapsed_time(f2)
+    out["commands"]["check_stress_fused"] = {
+        "GBps": round(m * 8 / ((tf + tcf) / 1e3) / 1e9, 1), "bytes": m * 8, "ms": round(tf + tcf, 4),
+        "gen_inject_GBps": round(m * 4 / (tf / 1e3) / 1e9, 1), "check_GBps": round(m * 4 / (tcf / 1e3) / 1e9, 1),
+        "mismatches": vf.mismatches, "max_abs": vf.max_abs, "argmax_abs": vf.argmax_abs,
+        "same_record_as_separate": (vf.mismatches, vf.max_abs, vf.argmax_abs, vf.nan_count)
+        == (v.mismatches, v.max_abs, v.argmax_abs, v.nan_count)}
     out["commands"]["check_stress"] = {
+        "ms": round(tg + ti + tc, 4),
         "GBps": round(nbytes / ((tg + ti + tc) / 1e3) / 1e9, 1), "bytes": nbytes,
         "gen_GBps": round(m * 2 / (tg / 1e3) / 1e9, 1), "inject_GBps": round(m * 4 / (ti / 1e3) / 1e9, 1),
         "check_GBps": round(m * 4 / (tc / 1e3) / 1e9, 1), "mismatches": v.mismatches, "max_abs": v.max_abs,

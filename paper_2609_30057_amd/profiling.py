@@ -103,6 +103,19 @@ def cmd_stats(a):
         f.write("\n".join(lines) + "\n")
 
 
+def default_algo(workload):
+    """Algorithmic bytes per launch of the bench command's kernels: the
+    generation writes n elements, the check reads both operands (bf16
+    candidate, fp32 reference), the flush writes its buffer."""
+    if workload != "gemm_large":
+        return {}
+    from . import workloads as W
+    cfg = W.GEMM_LARGE
+    n = cfg["n"] * cfg["n"]
+    return {"krex::k_gen<1, 1, false>": n * 2, "krex::k_check<1, 0, true, 2>": n * (2 + 4),
+            "krex::k_flush": cfg["flush_bytes"]}
+
+
 def cmd_traffic(a):
     fetch = counters(a.fetch, "FETCH_SIZE")
     write = counters(a.write, "WRITE_SIZE")
@@ -113,7 +126,7 @@ def cmd_traffic(a):
     f_copy = statistics.median(fetch[ck]) * 1024.0
     w_copy = statistics.median(write[ck]) * 1024.0
     sf, sw = GIB / f_copy, GIB / w_copy
-    algo = json.loads(a.algo) if a.algo else {}
+    algo = json.loads(a.algo) if a.algo else default_algo(a.workload)
     exact = {}
     if a.rdreq:
         parts = {sz: counters(a.rdreq, "TCC_EA0_RDREQ_%dB_sum" % sz) for sz in (32, 64, 128)}
@@ -164,7 +177,7 @@ def _unit_path(asm, kernel_symbol):
         raise KeyError(kernel_symbol)
     body = m.group(1).splitlines()
     start = next(i for i, l in enumerate(body) if "Loop Header" in l)
-    end = next(i for i, l in enumerate(body) if "global_store_dwordx4" in l)
+    end = next(i for i, l in enumerate(body) if re.search(r"\b(global|buffer)_store_dwordx4\b", l))
     ops = []
     for l in body[start:end + 1]:
         t = l.strip()
