@@ -299,6 +299,16 @@ def run_kernels():
     rec("check f16xf16 268M", t_ms(lambda: krex.check(y16, x16, 1e-3, 1e-3, out=out, sync=False)), x16.numel() * 4)
     rec("check f8xf8 268M", t_ms(lambda: krex.check(y8, x8, 0.125, 0.125, out=out, sync=False)), x8.numel() * 2)
     rec("check f32xf32 67M", t_ms(lambda: krex.check(yf, xf, 1e-4, 1e-5, out=out, sync=False)), xf.numel() * 8)
+    # the check against a regenerated reference reads the candidate only
+    rec("check_gen f16 vs f16 uniform 268M", t_ms(lambda: krex.check_gen(y16, torch.float16, 2, 1e-3, 1e-3, dist="uniform",
+                                                                          p0=-4.0, p1=4.0, out=out, sync=False)),
+        x16.numel() * 2)
+    rec("check_gen f8 vs f8 normal 268M", t_ms(lambda: krex.check_gen(y8, torch.float8_e4m3fn, 5, 0.125, 0.125,
+                                                                       dist="normal", out=out, sync=False)), x8.numel())
+    rec("check_gen f32 vs f32 uniform 67M", t_ms(lambda: krex.check_gen(yf, torch.float32, 7, 1e-4, 1e-5, out=out,
+                                                                         sync=False)), xf.numel() * 4)
+    rec("check_gen bf16 vs f32 normal 16.8M", t_ms(lambda: krex.check_gen(a_bf, torch.float32, 1, 1.6e-2, 1e-2,
+                                                                           dist="normal", out=out, sync=False)), N * 2)
     rec("flush 1GiB", t_ms(lambda: krex.flush(fl, 1)), GIB)
     return {"metric": "per-kernel throughput (algorithmic bytes / event time)", "unit": "GB/s",
             "peak_GBps": HBM_PEAK_GBPS, "kernels": res}

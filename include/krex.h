@@ -194,6 +194,19 @@ krex_status krex_gen_inject(void *x, void *y, int32_t dtype, uint64_t n, uint64_
 krex_status krex_check(const void *a, int32_t dta, const void *b, int32_t dtb, uint64_t n, float rtol,
                        float atol, krex_check_result *out, void *stream);
 
+/* The same check against a reference that is regenerated instead of read:
+ * *out equals krex_check(a, dta, b, dtb, n, rtol, atol) for the b that
+ * krex_gen(b, dtb, n, seed, offset, dist, p0, p1) writes, field for field,
+ * but b is never materialised: each reference element is recomputed from
+ * its Philox word (the reference of a benchmarking command whose expected
+ * output is itself a generated tensor, Section 1; Section 2.1), so only a is
+ * read from memory. Fastest when a is 16-byte aligned and offset is a
+ * multiple of 4. Arguments and errors as for krex_gen (dist, p0, p1, offset)
+ * and krex_check (a, dta, rtol, atol, n, out); dtb not KREX_U32. */
+krex_status krex_check_gen(const void *a, int32_t dta, int32_t dtb, uint64_t n, uint64_t seed, uint64_t offset,
+                           int32_t dist, float p0, float p1, float rtol, float atol, krex_check_result *out,
+                           void *stream);
+
 /* --- cache flush ------------------------------------------------------------
  * Writes `pattern` to every 32-bit word of buf[0..bytes) (device, 16-byte
  * aligned, bytes a multiple of 16) with stores that allocate in the

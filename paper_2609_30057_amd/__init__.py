@@ -112,6 +112,7 @@ def lib():
             "krex_inject": (i32, [vp, vp, i32, u64, u64, u64, f64, f32, i32, vp]),
             "krex_gen_inject": (i32, [vp, vp, i32, u64, u64, u64, i32, f32, f32, u64, u64, f64, f32, i32, vp]),
             "krex_check": (i32, [vp, i32, vp, i32, u64, f32, f32, vp, vp]),
+            "krex_check_gen": (i32, [vp, i32, i32, u64, u64, u64, i32, f32, f32, f32, f32, vp, vp]),
             "krex_flush": (i32, [vp, u64, u32, vp]),
             "krex_probe": (i32, [u64, vp, vp]),
             "krex_region_begin": (i32, [vp, u32, vp, u64]),
@@ -272,6 +273,26 @@ def check(a, b, rtol, atol, out=None, stream=None, sync=True):
         out = check_result_buffer(a.device)
     _chk(lib().krex_check(_dev(a), dtype_code(a.dtype), _dev(b), dtype_code(b.dtype), a.numel(), float(rtol),
                           float(atol), _dev(out), _stream(stream)), "krex_check")
+    if not sync:
+        return out
+    return decode_check_result(out)
+
+
+def check_gen(a, dtype_b, seed, rtol, atol, offset=0, dist="uniform", p0=None, p1=None, out=None, stream=None,
+              sync=True):
+    """check(a, b, rtol, atol) for the b that gen(b, seed, offset, dist, p0,
+    p1) would write into a tensor of dtype_b with a's size, regenerated
+    instead of read (only a is read). With sync=False returns the device
+    result buffer to decode later."""
+    d = _dist(dist)
+    if p0 is None:
+        p0 = -1.0 if d == UNIFORM else 0.0
+    if p1 is None:
+        p1 = 1.0 if d == UNIFORM else (1.0 if d == NORMAL else 0.0)
+    if out is None:
+        out = check_result_buffer(a.device)
+    _chk(lib().krex_check_gen(_dev(a), dtype_code(a.dtype), dtype_code(dtype_b), a.numel(), seed & (2**64 - 1), offset,
+                              d, p0, p1, float(rtol), float(atol), _dev(out), _stream(stream)), "krex_check_gen")
     if not sync:
         return out
     return decode_check_result(out)

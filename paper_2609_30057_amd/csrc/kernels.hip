@@ -29,29 +29,12 @@
 
 #include <cmath>
 
-#include <tuple>
-#include <utility>
-
+#include "check_device.hpp"
+#include "hip_launch.hpp"
 #include "krex_device.hpp"
 #include "launch.hpp"
 
 namespace krex {
-
-// hipLaunchKernel with the kernel's own parameter types, returning the
-// launch status directly instead of through the sticky last-error state.
-template <typename... KArgs, typename... Actual>
-static hipError_t launch(void (*kern)(KArgs...), dim3 grid, dim3 block, hipStream_t s, Actual &&...a)
-{
-    std::tuple<KArgs...> args(std::forward<Actual>(a)...);
-    void *argv[sizeof...(KArgs)];
-    std::apply([&](auto &...x) {
-        int i = 0;
-        ((argv[i++] = (void *)&x), ...);
-    }, args);
-    return hipLaunchKernel((const void *)kern, grid, block, argv, 0, s);
-}
-
-static constexpr int kThreads = 256;
 
 template <int DT> struct group_of { static constexpr int G = 4 / dtype_traits<DT>::size; };
 
@@ -131,14 +114,6 @@ static void shape(uint64_t units, uint32_t u_pref, uint32_t *U, uint32_t *grid)
     *grid = (uint32_t)(g ? g : 1);
 }
 
-static uint32_t tune_env(const char *name, uint32_t dflt)
-{
-    const char *e = getenv(name);
-    if (!e) return dflt;
-    const unsigned long v = strtoul(e, nullptr, 10);
-    return v ? (uint32_t)v : dflt;
-}
-
 // Whether range 2^-W times every integer f in [0, 2^W) is an exact fp32
 // product: range positive and finite, c = range 2^-W normal, and the odd part
 // q of range's 24-bit significand small enough that f q < 2^24 for every f
@@ -157,6 +132,18 @@ static bool exact_scale(float range, int W, float *c)
     if (!(cc >= FLT_MIN) || q * ((1ull << W) - 1ull) >= (1ull << 24)) return false;
     *c = cc;
     return true;
+}
+
+bool gen_transform_constants(int dist, float p0, float p1, float *q1)
+{
+    const float r = (dist == UNIFORM) ? (p1 - p0) : p1;
+    float c = 0.0f;
+    if (dist == UNIFORM && exact_scale(r, 24, &c)) {
+        *q1 = c;
+        return true;
+    }
+    *q1 = r;
+    return false;
 }
 
 template <int DT, int DIST>
@@ -743,380 +730,17 @@ hipError_t launch_gen_inject(void *x, void *y, int dt, uint64_t n, uint64_t seed
 
 // ---------------------------------------------------------------------- check
 //
-// Two launches and no atomics. k_check: block b owns chunks
-// [b 256 U, (b + 1) 256 U) of E elements (one 16-byte vector of the
-// narrower operand); thread t takes chunk b 256 U + u 256 + t for u < U, so
-// every step of a wave reads contiguous memory. Per element the verdict is
-// branch-free; mismatch and NaN counts are wave ballots summed on the scalar
-// unit; the per-lane maximum |a - b| is tracked per chunk, and the first
-// index of the wave's maximum is recovered at the end by its winning lane
-// re-reading that one chunk. Each block writes one
-// 32-byte partial with plain stores; k_check_final reduces the partials and
-// writes the result record.
-//
-// max_rel without a division per element: a lane keeps the pair (d*, b*)
-// with the largest exact ratio d / |b| among its elements with finite
-// positive d, comparing d b* > d* |b| in fp64, where the products of two
-// fp32 values are exact. One correctly rounded fp32 division per lane then
-// gives fl(max d / |b|), which equals max fl(d / |b|) because rounding is
-// monotone. Infinite d (an infinite operand, or overflow) enters as the pair
-// (inf, 0), ratio +inf.
-//
-// (A per-block atomic finish costs ~12 ns per same-address device atomic on
-// this GPU, serialised: 2048 blocks x 5 atomics is ~130 us, longer than
-// reading 100 MB.)
-
-static constexpr uint64_t kIdxMask = (1ull << 33) - 1;   // n < 2^33
-static constexpr int kMaxCheckBlocks = 4096;
-static constexpr int kFinalThreads = 256;
-
-struct CheckPartial {
-    uint64_t mism;
-    uint64_t nan;
-    uint64_t key;       // (bits(max d) << 33) | (kIdxMask - index); 0 = no NaN-free element
-    uint32_t rel_bits;  // max rel (non-negative fp32 bits)
-    uint32_t pad;
-};
-
-static_assert(sizeof(CheckPartial) == 32, "partial layout");
+// The kernel body, its building blocks and the reference sources live in
+// check_device.hpp; k_check takes the reference from memory.
 
 size_t check_scratch_bytes() { return (size_t)kMaxCheckBlocks * sizeof(CheckPartial); }
 
-struct LaneAcc {
-    uint32_t wmism, wnan;   // wave totals (exact in the wave's first lane)
-    float rd, rb;           // element with the largest ratio d / |b| (rb = 0: +inf)
-};
-
-__device__ __forceinline__ uint32_t popc(uint64_t m) { return (uint32_t)__builtin_popcountll(m); }
-
-// Every d > 0 has d / |b| >= 2^-26 (fp32 operands that differ are at least
-// one spacing of the nearer one apart, or |b| / 2 when far apart; b = 0 gives
-// +inf), so 2^-32 is a lower bound of any ratio that can raise a maximum
-// above its initial 0.
-static constexpr float kRatioFloor = 0x1p-32f;
-
-// Exact ratio update of one element: the pair (d, bn) replaces (rd, rb) when
-// d / bn > rd / rb, compared as d rb > rd bn in fp64 (products of two fp32
-// values are exact there). An infinite d enters as (inf, 0), ratio +inf, which no
-// later pair exceeds; d = 0 and NaN never compare greater.
-__device__ __forceinline__ void ratio_update(float A, float B, LaneAcc &acc)
-{
-    const float d0 = __builtin_fabsf(A - B);
-    const bool dinf = d0 == __builtin_inff();
-    const float bn = dinf ? 0.0f : __builtin_fabsf(B);
-    const bool greater = (double)d0 * (double)acc.rb > (double)acc.rd * (double)bn;
-    acc.rd = greater ? d0 : acc.rd;
-    acc.rb = greater ? bn : acc.rb;
-}
-
-// Counts and verdict of one element, accumulated as wave ballots of plain
-// comparisons (each lowers to one compare writing a lane mask). The element
-// mismatches when a != b (unordered included) and not d0 <= min(thr,
-// FLT_MAX): d0 is +inf exactly when the operands differ and one is infinite,
-// or their difference overflows, and is then never close; clamping the
-// threshold to the largest float excludes it in the same comparison (a NaN
-// threshold, 0 x inf, arises only with |b| = inf, where d0 is inf or NaN and
-// the verdict is a mismatch either way). CLAMP = false when neither operand
-// type has an infinity and their difference cannot overflow (fp8 e4m3fn
-// pairs: |a|, |b| <= 448): d0 is then never +inf and the threshold never
-// NaN, so the clamp cannot change a verdict.
-template <bool CLAMP = true>
-__device__ __forceinline__ uint64_t count_elem(float A, float B, float d0, float ab, float rtol, float atol,
-                                               LaneAcc &acc)
-{
-    const float rt = rtol * ab;
-    const float thr = CLAMP ? __builtin_fminf(atol + rt, 0x1.fffffep127f) : atol + rt;
-    const uint64_t ne = __ballot(A != B);
-    const uint64_t far = __ballot(!(d0 <= thr));
-    const uint64_t unord = __ballot(__builtin_isunordered(A, B));
-    acc.wmism += popc(ne & far);
-    acc.wnan += popc(unord);
-    return ne & ~unord;             // lanes whose operands are ordered and differ
-}
-
-// One element with its exact ratio update; returns d (0 when equal, NaN when
-// unordered) for the |a - b| maximum. Used for the n mod E tail.
-__device__ __forceinline__ float check_elem(float A, float B, float rtol, float atol, LaneAcc &acc)
-{
-    const float d0 = __builtin_fabsf(A - B);
-    count_elem(A, B, d0, __builtin_fabsf(B), rtol, atol, acc);
-    ratio_update(A, B, acc);
-    return (A == B) ? 0.0f : d0;
-}
-
-// The same d, for re-reading the best chunk.
-__device__ __forceinline__ float elem_d(float A, float B)
-{
-    return (A == B) ? 0.0f : __builtin_fabsf(A - B);
-}
-
-template <int DA, int DB, bool VEC>
-struct ChunkIO {
-    using TA = typename dtype_traits<DA>::storage;
-    using TB = typename dtype_traits<DB>::storage;
-    static constexpr int SA = dtype_traits<DA>::size;
-    static constexpr int SB = dtype_traits<DB>::size;
-    static constexpr int E = 16 / (SA < SB ? SA : SB);
-    static constexpr int VA = E * SA / 16;
-    static constexpr int VB = E * SB / 16;
-
-    // Raw bytes of one chunk: 16-byte vectors of each operand.
-    struct Raw {
-        union {
-            uint4 v[VA];
-            uint32_t w[4 * VA];
-            TA s[E];
-        } a;
-        union {
-            uint4 v[VB];
-            uint32_t w[4 * VB];
-            TB s[E];
-        } b;
-    };
-
-    __device__ __forceinline__ static void load_raw(const uint8_t *a, const uint8_t *b, uint64_t c, Raw &r)
-    {
-#pragma unroll
-        for (int i = 0; i < VA; ++i) r.a.v[i] = load16_stream(a + (c * VA + i) * 16);
-#pragma unroll
-        for (int i = 0; i < VB; ++i) r.b.v[i] = load16_stream(b + (c * VB + i) * 16);
-    }
-
-    // fp8 elements are converted two at a time straight from their 32-bit
-    // words (the packed converter's half-word select: no shifts or masks).
-    template <int DT, int NW>
-    __device__ __forceinline__ static void widen_words(const uint32_t (&w)[NW],
-                                                       const typename dtype_traits<DT>::storage (&s)[E], float (&X)[E])
-    {
-        if constexpr (DT == F8) {
-            typedef float f2 __attribute__((ext_vector_type(2)));
-#pragma unroll
-            for (int i = 0; i < NW; ++i) {
-                const f2 lo = __builtin_amdgcn_cvt_pk_f32_fp8((int)w[i], false);
-                const f2 hi = __builtin_amdgcn_cvt_pk_f32_fp8((int)w[i], true);
-                X[4 * i + 0] = lo.x;
-                X[4 * i + 1] = lo.y;
-                X[4 * i + 2] = hi.x;
-                X[4 * i + 3] = hi.y;
-            }
-        } else {
-#pragma unroll
-            for (int e = 0; e < E; ++e) X[e] = widen<DT>(s[e]);
-        }
-    }
-
-    __device__ __forceinline__ static void widen_raw(const Raw &r, float (&A)[E], float (&B)[E])
-    {
-        widen_words<DA, 4 * VA>(r.a.w, r.a.s, A);
-        widen_words<DB, 4 * VB>(r.b.w, r.b.s, B);
-    }
-
-    __device__ __forceinline__ static void load(const uint8_t *a, const uint8_t *b, uint64_t c, float (&A)[E],
-                                                float (&B)[E])
-    {
-        if constexpr (VEC) {
-            Raw r;
-            load_raw(a, b, c, r);
-            widen_raw(r, A, B);
-        } else {
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-                A[e] = widen<DA>(reinterpret_cast<const TA *>(a)[c * E + e]);
-                B[e] = widen<DB>(reinterpret_cast<const TB *>(b)[c * E + e]);
-            }
-        }
-    }
-};
-
-// max_rel with a wave-wide filter: R (wave-uniform) is a lower bound of the
-// largest exact ratio the wave holds. An element whose ratio is at least R
-// has d >= R |b| exactly, hence d >= fl(R |b|) (rounding is monotone and d
-// is a float); so an element with d < fl(R |b|) cannot raise the maximum and
-// skips the exact fp64 update. Only when some lane of the wave has a
-// candidate does the wave run the exact updates for the chunk and raise R to
-// the wave maximum of one-ulp-lowered fl(rd / rb). Only ordered, differing
-// elements are candidates; a NaN product (inf x 0) counts as one. Called by
-// every lane of the wave (the shuffles read
-// all lanes) with the wave's candidate mask; lanes without a chunk pass
-// valid = false.
-template <int E>
-struct RatioFilter {
-    float R = kRatioFloor;
-
-    __device__ __forceinline__ void chunk(const float (&A)[E], const float (&B)[E], bool valid, uint64_t cand,
-                                          LaneAcc &acc)
-    {
-        if (cand == 0) return;                  // wave-uniform
-        if (valid) {
-#pragma unroll
-            for (int e = 0; e < E; ++e) ratio_update(A[e], B[e], acc);
-        }
-        const float q = acc.rd / acc.rb;        // 0, a positive float, or +inf
-        float lo = (q > 0.0f && q < __builtin_inff()) ? __uint_as_float(__float_as_uint(q) - 1u) : q;
-#pragma unroll
-        for (int off = 32; off > 0; off >>= 1) lo = __builtin_fmaxf(lo, __shfl_xor(lo, off, 64));
-        lo = __uint_as_float(__builtin_amdgcn_readfirstlane(__float_as_uint(lo)));
-        R = __builtin_fmaxf(R, lo);
-    }
-};
-
+// Reference operand in memory.
 template <int DA, int DB, bool VEC, int D>
 __global__ __launch_bounds__(kThreads) void k_check(const uint8_t *a, const uint8_t *b, uint64_t n, float rtol,
                                                     float atol, CheckPartial *partials, uint32_t U)
 {
-    using IO = ChunkIO<DA, DB, VEC>;
-    constexpr int E = IO::E;
-    const uint32_t t = threadIdx.x;
-    const uint64_t nchunks = n / E;
-    const uint64_t base = (uint64_t)blockIdx.x * kThreads * U;
-    LaneAcc acc{0u, 0u, 0.0f, 1.0f};
-    RatioFilter<E> rf;
-    float best_d = -1.0f;               // largest non-NaN d seen by this lane
-    uint32_t best_c = 0;                // its chunk
-    // Counts and |a - b| maximum of one chunk; returns the lanes of the wave
-    // whose chunk has a max_rel candidate.
-    auto process = [&](const float (&A)[E], const float (&B)[E], uint64_t c) -> uint64_t {
-        float cmax = -1.0f;             // NaN d (unordered) is ignored by the maximum
-        uint64_t cand = 0;
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-            const float d0 = __builtin_fabsf(A[e] - B[e]);
-            const float ab = __builtin_fabsf(B[e]);
-            const uint64_t differ = count_elem<!(DA == F8 && DB == F8)>(A[e], B[e], d0, ab, rtol, atol, acc);
-            // Equal operands (ratio 0, or 0/0) and unordered ones (NaN d)
-            // never raise the maximum: only ordered, differing elements are
-            // candidates (otherwise every zero reference would be one).
-            cand |= __ballot(!(d0 < rf.R * ab)) & differ;
-            cmax = __builtin_fmaxf(cmax, (A[e] == B[e]) ? 0.0f : d0);
-        }
-        if (cmax > best_d) {
-            best_d = cmax;
-            best_c = (uint32_t)c;
-        }
-        return cand;
-    };
-    if constexpr (VEC) {
-        // Software pipeline over a ring of D chunk buffers: the loads of the
-        // next D - 1 chunks are in flight while the current one is
-        // evaluated. Every load is unconditional (a lane with nothing left
-        // re-reads the last chunk, which stays in L2), so the compiler's
-        // memory-counter waits stay exact: an evaluation waits for its own
-        // buffer only, never for the loads issued after it. A lane's chunks
-        // only grow with j, so the first lane of a wave holds a chunk
-        // whenever any lane does.
-        if (nchunks != 0) {
-            const uint64_t last = nchunks - 1;
-            auto cj = [&](uint32_t j) { return base + t + (uint64_t)j * kThreads; };
-            auto hj = [&](uint32_t j) { return j < U && cj(j) < nchunks; };
-            typename IO::Raw r[D];
-#pragma unroll
-            for (int k = 0; k < D - 1; ++k) IO::load_raw(a, b, hj(k) ? cj(k) : last, r[k]);
-            for (uint32_t u = 0; u < U; u += D) {
-#pragma unroll
-                for (int k = 0; k < D; ++k) {
-                    const uint32_t jn = u + k + D - 1;
-                    IO::load_raw(a, b, hj(jn) ? cj(jn) : last, r[(k + D - 1) % D]);
-                    const uint32_t j = u + k;
-                    const bool h = hj(j);
-                    float A[E], B[E];   // read only where h holds
-                    uint64_t cand = 0;
-                    if (h) {
-                        IO::widen_raw(r[k], A, B);
-                        cand = process(A, B, cj(j));
-                    }
-                    rf.chunk(A, B, h, cand, acc);
-                }
-            }
-        }
-    } else {
-        for (uint32_t u = 0; u < U; ++u) {
-            const uint64_t c = base + (uint64_t)u * kThreads + t;
-            const bool have = c < nchunks;
-            float A[E], B[E];           // read only where have holds
-            uint64_t cand = 0;
-            if (have) {
-                IO::load(a, b, c, A, B);
-                cand = process(A, B, c);
-            }
-            rf.chunk(A, B, have, cand, acc);
-        }
-    }
-    // The lane's candidate for the |a - b| maximum: best_d at position pos,
-    // the first index of its best chunk (the chunk holds the lane's first
-    // element attaining best_d), or a tail index.
-    uint64_t pos = (uint64_t)best_c * E;
-    bool in_chunk = true;
-    // The n mod E tail: the first block's first lanes, one element each.
-    const uint64_t tail0 = nchunks * E;
-    if (blockIdx.x == 0 && tail0 + t < n) {
-        const uint64_t i = tail0 + t;
-        const float A = widen<DA>(reinterpret_cast<const typename IO::TA *>(a)[i]);
-        const float B = widen<DB>(reinterpret_cast<const typename IO::TB *>(b)[i]);
-        const float d = check_elem(A, B, rtol, atol, acc);
-        if (d > best_d) {     // tail indices exceed every chunk index
-            best_d = d;
-            pos = i;
-            in_chunk = false;
-        }
-    }
-    // Only the wave's winner, the largest best_d at the lowest position,
-    // re-reads its chunk for the exact index (one chunk per wave, not per
-    // lane: a chunk's two operands span two 128-byte lines). Chunks are
-    // disjoint and ordered by position, so no other lane of the wave holds
-    // an element attaining best_d below the winner's chunk, and the exact
-    // key stays the wave's largest.
-    uint64_t key = best_d >= 0.0f ? (((uint64_t)__float_as_uint(best_d) << 33) | (kIdxMask - pos)) : 0ull;
-    uint64_t wkey = key;
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-        const uint64_t k2 = __shfl_xor((unsigned long long)wkey, off, 64);
-        wkey = k2 > wkey ? k2 : wkey;
-    }
-    if (key != 0 && key == wkey && in_chunk) {
-        float A[E], B[E];
-        IO::load(a, b, best_c, A, B);
-        uint64_t best_i = pos;
-        for (int e = E - 1; e >= 0; --e)
-            if (elem_d(A[e], B[e]) == best_d) best_i = pos + (uint64_t)e;
-        key = ((uint64_t)__float_as_uint(best_d) << 33) | (kIdxMask - best_i);
-    }
-    float rel = acc.rd / acc.rb;                 // +inf when rb = 0 < rd; 0 for the initial (0, 1)
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-        const uint64_t k2 = __shfl_xor((unsigned long long)key, off, 64);
-        key = k2 > key ? k2 : key;
-        const float r2 = __shfl_xor(rel, off, 64);
-        rel = r2 > rel ? r2 : rel;
-    }
-    const uint32_t wm = __shfl(acc.wmism, 0, 64), wn = __shfl(acc.wnan, 0, 64);
-    __shared__ uint64_t s_key[kThreads / 64];
-    __shared__ uint32_t s_m[kThreads / 64], s_n[kThreads / 64];
-    __shared__ float s_r[kThreads / 64];
-    const int w = t / 64;
-    if ((t & 63) == 0) {
-        s_key[w] = key;
-        s_m[w] = wm;
-        s_n[w] = wn;
-        s_r[w] = rel;
-    }
-    __syncthreads();
-    if (t == 0) {
-        CheckPartial p;
-        p.mism = 0;
-        p.nan = 0;
-        p.key = 0;
-        float r = 0.0f;
-#pragma unroll
-        for (int i = 0; i < kThreads / 64; ++i) {
-            p.mism += s_m[i];
-            p.nan += s_n[i];
-            p.key = s_key[i] > p.key ? s_key[i] : p.key;
-            r = s_r[i] > r ? s_r[i] : r;
-        }
-        p.rel_bits = __float_as_uint(r);
-        p.pad = 0;
-        partials[blockIdx.x] = p;
-    }
+    check_body<DA, DB, VEC, D>(a, RefMem<DB, chunk_elems<DA, DB>()>{b}, n, rtol, atol, partials, U);
 }
 
 __global__ __launch_bounds__(kFinalThreads) void k_check_final(const CheckPartial *partials, uint32_t nblocks,
@@ -1182,57 +806,33 @@ __global__ __launch_bounds__(kFinalThreads) void k_check_final(const CheckPartia
     }
 }
 
-// Blocks of k_check<DA, DB, VEC, D> the current device holds at once, capped
-// at the partial buffer's capacity; cached per device.
-template <int DA, int DB, bool VEC, int D>
-static uint32_t check_resident()
+hipError_t launch_check_final(const CheckPartial *partials, uint32_t nblocks, uint64_t n, krex_check_result *out,
+                              hipStream_t s)
 {
-    constexpr int kDevCache = 64;
-    static uint32_t cache[kDevCache] = {};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kDevCache) dev = -1;
-    if (dev >= 0 && cache[dev]) return cache[dev];
-    int per_cu = 0, cus = 0;
-    uint32_t r = kMaxCheckBlocks / 2;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_check<DA, DB, VEC, D>, kThreads, 0) == hipSuccess &&
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev < 0 ? 0 : dev) == hipSuccess &&
-        per_cu > 0 && cus > 0)
-        r = (uint32_t)per_cu * (uint32_t)cus;
-    if (r > (uint32_t)kMaxCheckBlocks) r = kMaxCheckBlocks;
-    if (dev >= 0) cache[dev] = r;
-    return r;
+    return launch(k_check_final, dim3(1), dim3(kFinalThreads), s, partials, nblocks, n, out);
 }
 
 template <int DA, int DB, int D>
 static hipError_t check_ab_d(const void *a, const void *b, uint64_t n, float rtol, float atol, void *scratch,
                              krex_check_result *out, hipStream_t s)
 {
-    constexpr int SA = dtype_traits<DA>::size, SB = dtype_traits<DB>::size;
-    constexpr int E = 16 / (SA < SB ? SA : SB);
+    constexpr int E = chunk_elems<DA, DB>();
     const bool vec = (((uintptr_t)a & 15u) == 0 && ((uintptr_t)b & 15u) == 0);
-    const uint64_t nchunks = n / E;
-    // One resident round: the grid is at most the number of blocks the
-    // device holds at once (occupancy x compute units), so no partial last
-    // round of blocks idles most of the chip. Chunks per thread: enough to
-    // cover n with that grid, and at least u_floor (the pipeline's depth per
-    // lane, and fewer partials for small n).
-    static const uint32_t u_floor = tune_env("KREX_CHECK_U", 8);
-    const uint64_t resident = vec ? check_resident<DA, DB, true, D>() : check_resident<DA, DB, false, 2>();
-    uint64_t U = (nchunks + (uint64_t)kThreads * resident - 1) / ((uint64_t)kThreads * resident);
-    if (U < u_floor) U = u_floor;
-    if (U == 0) U = 1;
-    uint64_t G = (nchunks + (uint64_t)kThreads * U - 1) / ((uint64_t)kThreads * U);
-    if (G == 0) G = 1;   // the tail alone
+    static uint32_t cache_vec[64] = {}, cache_el[64] = {};
+    const uint64_t resident = vec ? resident_blocks((const void *)k_check<DA, DB, true, D>, cache_vec)
+                                  : resident_blocks((const void *)k_check<DA, DB, false, 2>, cache_el);
+    uint32_t U, G;
+    check_grid(n / E, resident, &U, &G);
     CheckPartial *parts = (CheckPartial *)scratch;
     hipError_t e;
     if (vec)
-        e = launch(k_check<DA, DB, true, D>, dim3((uint32_t)G), dim3(kThreads), s, (const uint8_t *)a, (const uint8_t *)b,
-                   n, rtol, atol, parts, (uint32_t)U);
+        e = launch(k_check<DA, DB, true, D>, dim3(G), dim3(kThreads), s, (const uint8_t *)a, (const uint8_t *)b, n,
+                   rtol, atol, parts, U);
     else
-        e = launch(k_check<DA, DB, false, 2>, dim3((uint32_t)G), dim3(kThreads), s, (const uint8_t *)a,
-                   (const uint8_t *)b, n, rtol, atol, parts, (uint32_t)U);
+        e = launch(k_check<DA, DB, false, 2>, dim3(G), dim3(kThreads), s, (const uint8_t *)a, (const uint8_t *)b, n,
+                   rtol, atol, parts, U);
     if (e != hipSuccess) return e;
-    return launch(k_check_final, dim3(1), dim3(kFinalThreads), s, (const CheckPartial *)parts, (uint32_t)G, n, out);
+    return launch_check_final(parts, G, n, out, s);
 }
 
 // Depth of the load ring: a third buffer in flight pays for pairs of one-

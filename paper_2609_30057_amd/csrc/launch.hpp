@@ -13,6 +13,12 @@ namespace krex {
 // Compute units of the current device (cached per device).
 int device_cus();
 
+// Generation's transform constant for (dist, p0, p1): c = range 2^-24 when
+// the uniform range fl(p1 - p0) scales every 24-bit integer exactly (returns
+// true; the transform is then one fused multiply-add), else the range
+// (uniform) or p1 (normal, bitcast).
+bool gen_transform_constants(int dist, float p0, float p1, float *q1);
+
 // `p1` is the distribution's second parameter as given (upper bound or std).
 hipError_t launch_gen(void *dst, int dt, uint64_t n, uint64_t seed, uint64_t offset, int dist, float p0, float p1,
                       hipStream_t s);
@@ -33,6 +39,12 @@ hipError_t launch_gen_inject(void *x, void *y, int dt, uint64_t n, uint64_t seed
 size_t check_scratch_bytes();
 hipError_t launch_check(const void *a, int dta, const void *b, int dtb, uint64_t n, float rtol, float atol,
                         void *scratch, krex_check_result *out, hipStream_t s);
+// The check of a against the reference krex_gen would write for (dtb,
+// seed, offset, dist, p0, p1), regenerated instead of read; scratch as for
+// launch_check.
+hipError_t launch_check_gen(const void *a, int dta, int dtb, uint64_t n, uint64_t seed, uint64_t offset, int dist,
+                            float p0, float p1, float rtol, float atol, void *scratch, krex_check_result *out,
+                            hipStream_t s);
 hipError_t launch_flush(void *buf, uint64_t bytes, uint32_t pattern, hipStream_t s);
 hipError_t launch_probe(uint64_t iters, float *sink, hipStream_t s);
 hipError_t launch_sgemm(uint32_t M, uint32_t N, uint32_t K, const float *A, const float *B, float *C,

@@ -34,6 +34,7 @@ GIB = 1 << 30
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 KERNELS_HIP = os.path.join(ROOT, "paper_2609_30057_amd", "csrc", "kernels.hip")
 DEVICE_HPP = os.path.join(ROOT, "paper_2609_30057_amd", "csrc", "krex_device.hpp")
+CHECK_HPP = os.path.join(ROOT, "paper_2609_30057_amd", "csrc", "check_device.hpp")
 
 # kernels.hip is split into sections by "// ---- <name>" rules; a traffic
 # figure is tied to the source of its kernel's section (plus the device
@@ -50,9 +51,12 @@ def _sections(path):
 
 def kernel_source_sha(kernel):
     """sha256 of the source that defines `kernel` (short name, e.g. k_flush):
-    its section of kernels.hip plus what it uses of the device header (the
-    flush only its streaming stores, the others the whole header)."""
+    its section of kernels.hip plus what it uses of the device headers (the
+    flush only its streaming stores, the others the whole header; the check
+    also the check body's header)."""
     body = _sections(KERNELS_HIP)[SECTION_OF[kernel]]
+    if kernel in ("k_check", "k_check_final"):
+        body += open(CHECK_HPP).read()
     if kernel == "k_flush":
         body += _sections(DEVICE_HPP)["streaming memory"]
     elif kernel not in ("k_probe", "k_sgemm"):

@@ -95,6 +95,22 @@ def test_host_only_entry_points():
     assert L.krex_gen_packed(None, k.BF16, 0, 0, 0, 0, -1.0, 1.0, None) == k.OK
     assert L.krex_check(None, k.F32, None, k.F32, 4, -1.0, 0.0, ctypes.c_void_p(8), None) == k.EINVAL
     assert L.krex_check(None, k.F32, None, k.F32, 2**33, 0.0, 0.0, ctypes.c_void_p(8), None) == k.EINVAL
+    # the regenerated-reference check validates like generation and the check
+    assert L.krex_check_gen(None, k.F32, k.U32, 4, 0, 0, 0, -1.0, 1.0, 0.0, 0.0, ctypes.c_void_p(8), None) == k.EINVAL
+    assert L.krex_check_gen(None, k.F32, k.F16, 4, 0, 0, 0, 1.0, -1.0, 0.0, 0.0, ctypes.c_void_p(8), None) == k.EINVAL
+    assert L.krex_check_gen(None, k.F32, k.F16, 4, 0, 0, 1, 0.0, -1.0, 0.0, 0.0, ctypes.c_void_p(8), None) == k.EINVAL
+    assert L.krex_check_gen(None, k.F32, k.F16, 4, 0, 0, 0, -1.0, 1.0, float("nan"), 0.0, ctypes.c_void_p(8),
+                            None) == k.EINVAL
+    assert L.krex_check_gen(None, k.F32, k.F16, 2**33, 0, 0, 0, -1.0, 1.0, 0.0, 0.0, ctypes.c_void_p(8),
+                            None) == k.EINVAL
+    assert L.krex_check_gen(None, k.F32, k.F16, 4, 0, 2**64 - 2, 0, -1.0, 1.0, 0.0, 0.0, ctypes.c_void_p(8),
+                            None) == k.EINVAL
+    assert L.krex_check_gen(None, k.F32, k.F16, 4, 0, 0, 0, -1.0, 1.0, 0.0, 0.0, None, None) == k.EINVAL
+    assert L.krex_check_gen(None, k.F32, k.F16, 4, 0, 0, 0, -1.0, 1.0, 0.0, 0.0, ctypes.c_void_p(8), None) == k.EINVAL
+    assert L.krex_check_gen(ctypes.c_void_p(2), k.F32, k.F16, 4, 0, 0, 0, -1.0, 1.0, 0.0, 0.0, ctypes.c_void_p(8),
+                            None) == k.EALIGN
+    assert L.krex_check_gen(ctypes.c_void_p(16), k.F32, k.F16, 4, 0, 0, 0, -1.0, 1.0, 0.0, 0.0, ctypes.c_void_p(12),
+                            None) == k.EALIGN
     assert L.krex_inject(None, None, k.F16, 4, 0, 0, 1.5, 0.5, 1, None) == k.EINVAL
     assert L.krex_flush(None, 17, 0, None) == k.EINVAL
     assert L.krex_region_begin(None, 10, None, 0) == k.ENOTATTACHED
