@@ -80,39 +80,49 @@ __device__ __forceinline__ void ratio_update(float A, float B, LaneAcc &acc)
     acc.rb = greater ? bn : acc.rb;
 }
 
-// Counts and verdict of one element, accumulated as wave ballots of plain
-// comparisons (each lowers to one compare writing a lane mask). The element
-// mismatches when a != b (unordered included) and not d0 <= min(thr,
-// FLT_MAX): d0 is +inf exactly when the operands differ and one is infinite,
-// or their difference overflows, and is then never close; clamping the
-// threshold to the largest float excludes it in the same comparison (a NaN
-// threshold, 0 x inf, arises only with |b| = inf, where d0 is inf or NaN and
-// the verdict is a mismatch either way). CLAMP = false when neither operand
-// type has an infinity and their difference cannot overflow (fp8 e4m3fn
-// pairs: |a|, |b| <= 448): d0 is then never +inf and the threshold never
-// NaN, so the clamp cannot change a verdict.
-template <bool CLAMP = true>
-__device__ __forceinline__ uint64_t count_elem(float A, float B, float d0, float ab, float rtol, float atol,
-                                               LaneAcc &acc)
-{
-    const float rt = rtol * ab;
-    const float thr = CLAMP ? __builtin_fminf(atol + rt, 0x1.fffffep127f) : atol + rt;
-    const uint64_t ne = __ballot(A != B);
-    const uint64_t far = __ballot(!(d0 <= thr));
-    const uint64_t unord = __ballot(__builtin_isunordered(A, B));
-    acc.wmism += popc(ne & far);
-    acc.wnan += popc(unord);
-    return ne & ~unord;             // lanes whose operands are ordered and differ
-}
+// The smallest positive fp32 value (denormals are kept): d > 0 exactly when
+// d >= kMinPositive.
+static constexpr float kMinPositive = 0x1p-149f;
 
-// One element with its exact ratio update; returns d (0 when equal, NaN when
-// unordered) for the |a - b| maximum. Used for the n mod E tail.
-__device__ __forceinline__ float check_elem(float A, float B, float rtol, float atol, LaneAcc &acc)
+// Verdict of one element as wave ballots (each comparison lowers to one
+// compare writing a lane mask). d is 0 when a == b (an infinity equal to
+// itself included), NaN when the pair is unordered, else |a - b|. The
+// element mismatches exactly when not d <= min(atol + rtol |b|, FLT_MAX): an
+// equal pair has d = 0, below any threshold (atol, rtol >= 0; a NaN
+// threshold, 0 x inf with |b| = inf, becomes FLT_MAX); an unordered pair has
+// d = NaN, never <= anything; a differing pair is close exactly when d is
+// finite and within the threshold (d = +inf, an infinite operand or an
+// overflowing difference, exceeds FLT_MAX). It is a max_rel candidate when
+// d >= max(fl(R |b|), kMinPositive), i.e. it differs, is ordered and its
+// ratio may reach R (the filter's bound; R |b| is NaN only for an unordered
+// pair). NOINF: neither operand type has an infinity and their difference
+// cannot overflow (fp8 e4m3fn pairs: |a|, |b| <= 448), so |a - b| is already
+// 0 for equal operands and the threshold is finite: no select, no clamp.
+// Mismatches are counted here; unordered pairs are counted by the caller.
+template <bool NOINF>
+__device__ __forceinline__ float elem_verdict(float A, float B, float rtol, float atol, float R, LaneAcc &acc,
+                                              uint64_t &cand)
 {
     const float d0 = __builtin_fabsf(A - B);
-    count_elem(A, B, d0, __builtin_fabsf(B), rtol, atol, acc);
+    const float ab = __builtin_fabsf(B);
+    const float d = NOINF ? d0 : ((A == B) ? 0.0f : d0);
+    const float rt = rtol * ab;
+    const float thr = NOINF ? atol + rt : __builtin_fminf(atol + rt, 0x1.fffffep127f);
+    acc.wmism += popc(__ballot(!(d <= thr)));
+    cand |= __ballot(d >= __builtin_fmaxf(R * ab, kMinPositive));
+    return d;
+}
+
+// One element with its exact ratio update and unordered count; returns d.
+// Used for the n mod E tail.
+template <bool NOINF>
+__device__ __forceinline__ float check_elem(float A, float B, float rtol, float atol, LaneAcc &acc)
+{
+    uint64_t cand = 0;
+    const float d = elem_verdict<NOINF>(A, B, rtol, atol, kRatioFloor, acc, cand);
+    acc.wnan += popc(__ballot(__builtin_isunordered(A, B)));
     ratio_update(A, B, acc);
-    return (A == B) ? 0.0f : d0;
+    return d;
 }
 
 // The same d, for re-reading the best chunk.
@@ -222,7 +232,7 @@ struct RefGen {
     static constexpr int NW = E * dtype_traits<DB>::size / 4;
     struct Raw {};
     uint64_t offset;    // word of element 0
-    uint32_t k0, k1;    // Philox key (the seed)
+    RoundKeys rk;       // the seed's Philox key schedule
     float p0, p1;
     uint32_t shift;     // offset mod 4
 
@@ -244,7 +254,7 @@ struct RefGen {
         const uint64_t b0 = (offset >> 2) + c * (E / 4);
         float v[E];
 #pragma unroll
-        for (int k = 0; k < E / 4; ++k) transform4<DIST, POW2>(philox_block(b0 + k, k0, k1), p0, p1, v + 4 * k);
+        for (int k = 0; k < E / 4; ++k) transform4<DIST, POW2>(philox_block(b0 + k, rk), p0, p1, v + 4 * k);
         finish(v, B);
     }
     // Any offset: the E / 4 + 1 blocks the chunk's words touch, the values
@@ -254,7 +264,7 @@ struct RefGen {
         const uint64_t b0 = (offset >> 2) + c * (E / 4);
         float v[E + 4];
 #pragma unroll
-        for (int k = 0; k < E / 4 + 1; ++k) transform4<DIST, POW2>(philox_block(b0 + k, k0, k1), p0, p1, v + 4 * k);
+        for (int k = 0; k < E / 4 + 1; ++k) transform4<DIST, POW2>(philox_block(b0 + k, rk), p0, p1, v + 4 * k);
         float x[E];
 #pragma unroll
         for (int e = 0; e < E; ++e)
@@ -265,7 +275,7 @@ struct RefGen {
     {
         const uint64_t w = offset + i;
         float v[4];
-        transform4<DIST, POW2>(philox_block(w >> 2, k0, k1), p0, p1, v);
+        transform4<DIST, POW2>(philox_block(w >> 2, rk), p0, p1, v);
         const uint32_t l = (uint32_t)w & 3u;
         const float x = l == 0 ? v[0] : l == 1 ? v[1] : l == 2 ? v[2] : v[3];
         return widen<DB>(narrow<DB, DIST == BITCAST>(x));
@@ -339,21 +349,24 @@ __device__ __forceinline__ void check_body(const uint8_t *a, const Ref &ref, uin
     RatioFilter<E> rf;
     float best_d = -1.0f;               // largest non-NaN d seen by this lane
     uint32_t best_c = 0;                // its chunk
+    constexpr bool NOINF = DA == F8 && DB == F8;
     // Counts and |a - b| maximum of one chunk; returns the lanes of the wave
-    // whose chunk has a max_rel candidate.
+    // whose chunk has a max_rel candidate. Unordered pairs are rare: a sum
+    // of the chunk's d (non-negative, so NaN exactly when some pair is
+    // unordered) decides per wave whether to count them.
     auto process = [&](const float (&A)[E], const float (&B)[E], uint64_t c) -> uint64_t {
         float cmax = -1.0f;             // NaN d (unordered) is ignored by the maximum
+        float dsum = 0.0f;
         uint64_t cand = 0;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-            const float d0 = __builtin_fabsf(A[e] - B[e]);
-            const float ab = __builtin_fabsf(B[e]);
-            const uint64_t differ = count_elem<!(DA == F8 && DB == F8)>(A[e], B[e], d0, ab, rtol, atol, acc);
-            // Equal operands (ratio 0, or 0/0) and unordered ones (NaN d)
-            // never raise the maximum: only ordered, differing elements are
-            // candidates (otherwise every zero reference would be one).
-            cand |= __ballot(!(d0 < rf.R * ab)) & differ;
-            cmax = __builtin_fmaxf(cmax, (A[e] == B[e]) ? 0.0f : d0);
+            const float d = elem_verdict<NOINF>(A[e], B[e], rtol, atol, rf.R, acc, cand);
+            dsum += d;
+            cmax = __builtin_fmaxf(cmax, d);
+        }
+        if (__ballot(dsum != dsum) != 0) {
+#pragma unroll
+            for (int e = 0; e < E; ++e) acc.wnan += popc(__ballot(__builtin_isunordered(A[e], B[e])));
         }
         if (cmax > best_d) {
             best_d = cmax;
@@ -423,7 +436,7 @@ __device__ __forceinline__ void check_body(const uint8_t *a, const Ref &ref, uin
         const uint64_t i = tail0 + t;
         const float A = CA::elem(a, i);
         const float B = ref.elem(i);
-        const float d = check_elem(A, B, rtol, atol, acc);
+        const float d = check_elem<NOINF>(A, B, rtol, atol, acc);
         if (d > best_d) {     // tail indices exceed every chunk index
             best_d = d;
             pos = i;

@@ -50,8 +50,7 @@ hipError_t check_gen_t(const void *a, const GenRefArgs &g, uint64_t n, float rto
 {
     constexpr int E = chunk_elems<DA, DB>();
     constexpr int D = kGenCheckDepth;
-    const RefGen<DB, DIST, POW2, E> ref{g.offset, (uint32_t)g.seed, (uint32_t)(g.seed >> 32), g.p0, g.p1,
-                                        (uint32_t)(g.offset & 3u)};
+    const RefGen<DB, DIST, POW2, E> ref{g.offset, round_keys(g.seed), g.p0, g.p1, (uint32_t)(g.offset & 3u)};
     const bool vec = ((uintptr_t)a & 15u) == 0 && (g.offset & 3u) == 0;
     static uint32_t cache_vec[64] = {}, cache_el[64] = {};
     const uint64_t resident = vec ? resident_blocks((const void *)k_check_gen<DA, DB, DIST, POW2, true, D>, cache_vec)

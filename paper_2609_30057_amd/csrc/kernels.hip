@@ -44,7 +44,6 @@ struct GenParams {
     uint8_t *dst;
     uint64_t n;
     uint64_t offset;
-    uint32_t k0, k1;
     float p0, p1;      // uniform: lo and fl(hi - lo); normal: mean and std
     float c;           // uniform with a power-of-two range: range 2^-24
     int pow2;          // uniform range is a power of two (c normal)
@@ -52,6 +51,7 @@ struct GenParams {
     uint64_t ngroups;  // groups of G blocks
     uint32_t U;        // groups per thread, block-contiguous
     int vec;           // offset % 4 == 0 and dst 16-byte aligned
+    RoundKeys rk;      // the seed's Philox key schedule
 };
 
 // POW2: uniform with a power-of-two range (the fused transform; P.c).
@@ -61,33 +61,54 @@ __global__ __launch_bounds__(kThreads) void k_gen(GenParams P)
     using T = typename dtype_traits<DT>::storage;
     constexpr int ES = dtype_traits<DT>::size;
     constexpr int G = group_of<DT>::G;
-    for (uint32_t u = 0; u < P.U; ++u) {
-        const uint64_t g = ((uint64_t)blockIdx.x * P.U + u) * kThreads + threadIdx.x;
-        if (g >= P.ngroups) break;
+    union Pack {
+        uint4 v;
+        uint32_t w[4];
+        T s[4 * G];
+    };
+    // Group g: G Philox blocks from P.b0 + g G, transformed and packed into
+    // 16 bytes.
+    auto group = [&](uint64_t g, Pack &pk) {
         const uint64_t bfirst = P.b0 + g * G;
-        union {
-            uint4 v;
-            uint32_t w[4];
-            T s[4 * G];
-        } pk;
         if constexpr (DT == U32) {
-            const words4 w = philox_block(bfirst, P.k0, P.k1);
+            const words4 w = philox_block(bfirst, P.rk);
 #pragma unroll
             for (int l = 0; l < 4; ++l) pk.w[l] = w.v[l];
         } else {
             words4 wb[G];
 #pragma unroll
-            for (int i = 0; i < G; ++i) wb[i] = philox_block(bfirst + i, P.k0, P.k1);
+            for (int i = 0; i < G; ++i) wb[i] = philox_block(bfirst + i, P.rk);
             float v[4 * G];
 #pragma unroll
             for (int i = 0; i < G; ++i) transform4<DIST, POW2>(wb[i], P.p0, POW2 ? P.c : P.p1, v + 4 * i);
             pack_narrow<DT, DIST == BITCAST>(v, pk.w);
         }
+    };
+    const uint64_t gb0 = (uint64_t)blockIdx.x * P.U * kThreads;   // the block's first group
+    const uint64_t gend = gb0 + (uint64_t)P.U * kThreads;
+    // vec: offset % 4 == 0, so group g's first element is 4 G g. A block whose
+    // groups all lie in range takes the path without per-lane checks (a
+    // block-uniform branch); only the grid's last block can miss it.
+    if (P.vec && gend <= P.ngroups && 4 * G * gend <= P.n) {
+        for (uint32_t u = 0; u < P.U; ++u) {
+            const uint64_t gb = gb0 + (uint64_t)u * kThreads;
+            Pack pk;
+            group(gb + threadIdx.x, pk);
+            store16_stream(P.dst + 4 * G * gb * ES, 16u * threadIdx.x, pk.v);
+        }
+        return;
+    }
+    for (uint32_t u = 0; u < P.U; ++u) {
+        const uint64_t g = gb0 + (uint64_t)u * kThreads + threadIdx.x;
+        if (g >= P.ngroups) break;
+        const uint64_t bfirst = P.b0 + g * G;
+        Pack pk;
+        group(g, pk);
         const uint64_t j0 = 4 * bfirst - P.offset;
         if (P.vec && j0 + 4 * G <= P.n) {
-            // vec: offset % 4 == 0; the block's first group starts at element
-            // jb (uniform across the block) and lane t's 16 bytes at jb + 4 G t
-            const uint64_t gb = ((uint64_t)blockIdx.x * P.U + u) * kThreads;
+            // the block's first group starts at element jb (uniform across
+            // the block) and lane t's 16 bytes at jb + 4 G t
+            const uint64_t gb = gb0 + (uint64_t)u * kThreads;
             const uint64_t jb = 4 * (P.b0 + gb * G) - P.offset;
             store16_stream(P.dst + jb * ES, 16u * threadIdx.x, pk.v);
         } else {
@@ -177,8 +198,6 @@ static GenParams make_gen_params(void *dst, int dt, uint64_t n, uint64_t seed, u
     P.dst = (uint8_t *)dst;
     P.n = n;
     P.offset = offset;
-    P.k0 = (uint32_t)seed;
-    P.k1 = (uint32_t)(seed >> 32);
     P.p0 = p0;
     P.p1 = (dist == UNIFORM) ? (p1 - p0) : p1;
     P.pow2 = (dist == UNIFORM && exact_scale(P.p1, 24, &P.c)) ? 1 : 0;
@@ -194,6 +213,7 @@ static GenParams make_gen_params(void *dst, int dt, uint64_t n, uint64_t seed, u
     P.ngroups = (nblocks + (uint64_t)G - 1) / (uint64_t)G;
     P.vec = ((offset & 3u) == 0 && ((uintptr_t)dst & 15u) == 0) ? 1 : 0;
     P.U = 1;
+    P.rk = round_keys(seed);
     return P;
 }
 
@@ -235,7 +255,6 @@ struct PackedParams {
     uint8_t *dst;
     uint64_t n;
     uint64_t offset;   // in fields
-    uint32_t k0, k1;
     float p0, p1;      // uniform: lo and fl(hi - lo); normal: mean and std
     float rs;          // uniform: fl(hi - lo) 2^-W when that is exact
     int umode;         // uniform: UM_WORD, UM_SCALED or UM_FUSED
@@ -243,6 +262,7 @@ struct PackedParams {
     uint64_t nunits;
     uint32_t U;        // units per thread, block-contiguous
     int vec;           // offset % E == 0 and dst 16-byte aligned
+    RoundKeys rk;      // the seed's Philox key schedule
 };
 
 // Uniform transform of a W-bit field f: UM_WORD applies the word-stream
@@ -262,22 +282,21 @@ __global__ __launch_bounds__(kThreads) void k_gen_packed(PackedParams P)
     constexpr int E = packed_of<DT, DIST>::E;
     constexpr int GB = packed_of<DT, DIST>::GB;
     constexpr uint32_t kMask = (1u << W) - 1u;
-    for (uint32_t u = 0; u < P.U; ++u) {
-        const uint64_t g = ((uint64_t)blockIdx.x * P.U + u) * kThreads + threadIdx.x;
-        if (g >= P.nunits) break;
-        const uint64_t unit = P.u0 + g;
+    union Pack {
+        uint4 v;
+        uint32_t w[4];
+        T s[E];
+    };
+    // Unit u0 + g: GB Philox blocks, E fields transformed and packed into
+    // 16 bytes.
+    auto unit_values = [&](uint64_t unit, Pack &pk) {
         uint32_t wv[4 * GB];
 #pragma unroll
         for (int i = 0; i < GB; ++i) {
-            const words4 w = philox_block(unit * GB + i, P.k0, P.k1);
+            const words4 w = philox_block(unit * GB + i, P.rk);
 #pragma unroll
             for (int l = 0; l < 4; ++l) wv[4 * i + l] = w.v[l];
         }
-        union {
-            uint4 v;
-            uint32_t w[4];
-            T s[E];
-        } pk;
         if constexpr (DIST == BITCAST) {
             static_assert(GB == 1, "bitcast units are one block");
 #pragma unroll
@@ -321,9 +340,30 @@ __global__ __launch_bounds__(kThreads) void k_gen_packed(PackedParams P)
             }
             pack_narrow<DT, false>(v, pk.w);
         }
+    };
+    const uint64_t gb0 = (uint64_t)blockIdx.x * P.U * kThreads;   // the block's first unit (from u0)
+    const uint64_t gend = gb0 + (uint64_t)P.U * kThreads;
+    // vec: offset % E == 0, so unit u0 + g starts at field E g. A block whose
+    // units all lie in range stores without per-lane checks (a block-uniform
+    // branch); only the grid's last block can miss it.
+    if (P.vec && gend <= P.nunits && E * gend <= P.n) {
+        for (uint32_t u = 0; u < P.U; ++u) {
+            const uint64_t gb = gb0 + (uint64_t)u * kThreads;
+            Pack pk;
+            unit_values(P.u0 + gb + threadIdx.x, pk);
+            store16_stream(P.dst + E * gb * ES, 16u * threadIdx.x, pk.v);
+        }
+        return;
+    }
+    for (uint32_t u = 0; u < P.U; ++u) {
+        const uint64_t g = gb0 + (uint64_t)u * kThreads + threadIdx.x;
+        if (g >= P.nunits) break;
+        const uint64_t unit = P.u0 + g;
+        Pack pk;
+        unit_values(unit, pk);
         const uint64_t q0 = unit * (uint64_t)E;
         if (P.vec && q0 >= P.offset && q0 - P.offset + E <= P.n) {
-            const uint64_t gb = ((uint64_t)blockIdx.x * P.U + u) * kThreads;
+            const uint64_t gb = gb0 + (uint64_t)u * kThreads;
             const uint64_t qb = (P.u0 + gb) * (uint64_t)E - P.offset;
             store16_stream(P.dst + qb * ES, 16u * threadIdx.x, pk.v);
         } else {
@@ -378,8 +418,7 @@ hipError_t launch_gen_packed(void *dst, int dt, uint64_t n, uint64_t seed, uint6
     P.dst = (uint8_t *)dst;
     P.n = n;
     P.offset = offset;
-    P.k0 = (uint32_t)seed;
-    P.k1 = (uint32_t)(seed >> 32);
+    P.rk = round_keys(seed);
     P.p0 = p0;
     P.p1 = (dist == UNIFORM) ? (p1 - p0) : p1;
     switch (dt) {
@@ -508,13 +547,13 @@ struct InjectParams {
     const uint8_t *x;
     uint64_t n;
     uint64_t moff;
-    uint32_t k0, k1;
     uint64_t T;        // threshold in [0, 2^32]
     float delta;
     uint64_t b0;
     uint64_t ngroups;
     uint32_t U;
     int vec;
+    RoundKeys rk;      // the mask seed's Philox key schedule
 };
 
 template <int DT, int MODE>
@@ -542,30 +581,52 @@ __global__ __launch_bounds__(kThreads) void k_inject(InjectParams P)
     using T = typename dtype_traits<DT>::storage;
     constexpr int ES = dtype_traits<DT>::size;
     constexpr int G = group_of<DT>::G;
+    union Pack {
+        uint4 v;
+        T s[4 * G];
+    };
+    // The 4 G elements from the group starting at Philox block bfirst,
+    // perturbed where their mask word is below T.
+    auto mask_group = [&](uint64_t bfirst, Pack &pk) {
+#pragma unroll
+        for (int i = 0; i < G; ++i) {
+            const words4 w = philox_block(bfirst + i, P.rk);
+#pragma unroll
+            for (int l = 0; l < 4; ++l)
+                if ((uint64_t)w.v[l] < P.T) pk.s[4 * i + l] = perturb<DT, MODE>(pk.s[4 * i + l], P.delta);
+        }
+    };
+    const uint64_t gb0 = (uint64_t)blockIdx.x * P.U * kThreads;   // the block's first group
+    const uint64_t gend = gb0 + (uint64_t)P.U * kThreads;
+    // vec: moff % 4 == 0, so group g's first element is 4 G g. A block whose
+    // groups all lie in range takes the path without per-lane checks (a
+    // block-uniform branch); only the grid's last block can miss it.
+    if (P.vec && gend <= P.ngroups && 4 * G * gend <= P.n) {
+        for (uint32_t u = 0; u < P.U; ++u) {
+            const uint64_t gb = gb0 + (uint64_t)u * kThreads;
+            const uint64_t g = gb + threadIdx.x;
+            Pack pk;
+            pk.v = load16_stream(P.x + 4 * G * g * ES);
+            mask_group(P.b0 + g * G, pk);
+            store16_stream(P.y + 4 * G * gb * ES, 16u * threadIdx.x, pk.v);
+        }
+        return;
+    }
     for (uint32_t u = 0; u < P.U; ++u) {
-        const uint64_t g = ((uint64_t)blockIdx.x * P.U + u) * kThreads + threadIdx.x;
+        const uint64_t g = gb0 + (uint64_t)u * kThreads + threadIdx.x;
         if (g >= P.ngroups) break;
         const uint64_t bfirst = P.b0 + g * G;
         const uint64_t j0 = 4 * bfirst - P.moff;
         if (P.vec && j0 + 4 * G <= P.n) {
-            union {
-                uint4 v;
-                T s[4 * G];
-            } pk;
+            Pack pk;
             pk.v = load16_stream(P.x + j0 * ES);
-#pragma unroll
-            for (int i = 0; i < G; ++i) {
-                const words4 w = philox_block(bfirst + i, P.k0, P.k1);
-#pragma unroll
-                for (int l = 0; l < 4; ++l)
-                    if ((uint64_t)w.v[l] < P.T) pk.s[4 * i + l] = perturb<DT, MODE>(pk.s[4 * i + l], P.delta);
-            }
-            const uint64_t gb = ((uint64_t)blockIdx.x * P.U + u) * kThreads;
+            mask_group(bfirst, pk);
+            const uint64_t gb = gb0 + (uint64_t)u * kThreads;
             const uint64_t jb = 4 * (P.b0 + gb * G) - P.moff;
             store16_stream(P.y + jb * ES, 16u * threadIdx.x, pk.v);
         } else {
             for (int i = 0; i < G; ++i) {
-                const words4 w = philox_block(bfirst + i, P.k0, P.k1);
+                const words4 w = philox_block(bfirst + i, P.rk);
                 for (int l = 0; l < 4; ++l) {
                     const uint64_t wi = 4 * (bfirst + i) + (uint64_t)l;
                     if (wi < P.moff || wi - P.moff >= P.n) continue;
@@ -598,8 +659,7 @@ hipError_t launch_inject(void *y, const void *x, int dt, uint64_t n, uint64_t ms
     P.x = (const uint8_t *)x;
     P.n = n;
     P.moff = moff;
-    P.k0 = (uint32_t)mseed;
-    P.k1 = (uint32_t)(mseed >> 32);
+    P.rk = round_keys(mseed);
     P.T = T;
     P.delta = delta;
     P.b0 = moff >> 2;
@@ -629,10 +689,10 @@ hipError_t launch_inject(void *y, const void *x, int dt, uint64_t n, uint64_t ms
 struct GenInjectParams {
     GenParams g;       // generation of x (offset % 4 == 0)
     uint8_t *y;
-    uint32_t m0, m1;   // mask key
     uint64_t mb0;      // first mask block: mask offset / 4
     uint64_t T;        // threshold in [0, 2^32]
     float delta;
+    RoundKeys mrk;     // the mask key's schedule
 };
 
 template <int DT, int DIST, bool POW2, int MODE>
@@ -642,35 +702,54 @@ __global__ __launch_bounds__(kThreads) void k_gen_inject(GenInjectParams Q)
     constexpr int ES = dtype_traits<DT>::size;
     constexpr int G = group_of<DT>::G;
     const GenParams &P = Q.g;
-    for (uint32_t u = 0; u < P.U; ++u) {
-        const uint64_t g = ((uint64_t)blockIdx.x * P.U + u) * kThreads + threadIdx.x;
-        if (g >= P.ngroups) break;
+    union Pack {
+        uint4 v;
+        uint32_t w[4];
+        T s[4 * G];
+    };
+    // Group g of x (G value blocks from P.b0 + g G) and of y (x perturbed
+    // where the mask words from Q.mb0 + g G are below T).
+    auto group = [&](uint64_t g, Pack &px, Pack &py) {
         const uint64_t bfirst = P.b0 + g * G;
         const uint64_t mfirst = Q.mb0 + g * G;
-        union {
-            uint4 v;
-            uint32_t w[4];
-            T s[4 * G];
-        } px, py;
         float v[4 * G];
 #pragma unroll
         for (int i = 0; i < G; ++i)
-            transform4<DIST, POW2>(philox_block(bfirst + i, P.k0, P.k1), P.p0, POW2 ? P.c : P.p1, v + 4 * i);
+            transform4<DIST, POW2>(philox_block(bfirst + i, P.rk), P.p0, POW2 ? P.c : P.p1, v + 4 * i);
         pack_narrow<DT, DIST == BITCAST>(v, px.w);
         py.v = px.v;
 #pragma unroll
         for (int i = 0; i < G; ++i) {
-            const words4 m = philox_block(mfirst + i, Q.m0, Q.m1);
+            const words4 m = philox_block(mfirst + i, Q.mrk);
 #pragma unroll
             for (int l = 0; l < 4; ++l)
                 if ((uint64_t)m.v[l] < Q.T) py.s[4 * i + l] = perturb<DT, MODE>(py.s[4 * i + l], Q.delta);
         }
-        const uint64_t j0 = 4 * bfirst - P.offset;
-        if (P.vec && j0 + 4 * G <= P.n) {
-            const uint64_t gb = ((uint64_t)blockIdx.x * P.U + u) * kThreads;
-            const uint64_t jb = 4 * (P.b0 + gb * G) - P.offset;
-            store16_stream(P.dst + jb * ES, 16u * threadIdx.x, px.v);
-            store16_stream(Q.y + jb * ES, 16u * threadIdx.x, py.v);
+    };
+    // offset % 4 == 0 (the launcher guarantees it), so group g's first
+    // element is 4 G g; blocks wholly in range store without per-lane checks.
+    const uint64_t gb0 = (uint64_t)blockIdx.x * P.U * kThreads;
+    const uint64_t gend = gb0 + (uint64_t)P.U * kThreads;
+    if (gend <= P.ngroups && 4 * G * gend <= P.n) {
+        for (uint32_t u = 0; u < P.U; ++u) {
+            const uint64_t gb = gb0 + (uint64_t)u * kThreads;
+            Pack px, py;
+            group(gb + threadIdx.x, px, py);
+            store16_stream(P.dst + 4 * G * gb * ES, 16u * threadIdx.x, px.v);
+            store16_stream(Q.y + 4 * G * gb * ES, 16u * threadIdx.x, py.v);
+        }
+        return;
+    }
+    for (uint32_t u = 0; u < P.U; ++u) {
+        const uint64_t g = gb0 + (uint64_t)u * kThreads + threadIdx.x;
+        if (g >= P.ngroups) break;
+        Pack px, py;
+        group(g, px, py);
+        const uint64_t j0 = 4 * G * g;
+        if (j0 + 4 * G <= P.n) {
+            const uint64_t gb = gb0 + (uint64_t)u * kThreads;
+            store16_stream(P.dst + 4 * G * gb * ES, 16u * threadIdx.x, px.v);
+            store16_stream(Q.y + 4 * G * gb * ES, 16u * threadIdx.x, py.v);
         } else {
             for (int e = 0; e < 4 * G; ++e) {
                 const uint64_t j = j0 + (uint64_t)e;
@@ -715,9 +794,8 @@ hipError_t launch_gen_inject(void *x, void *y, int dt, uint64_t n, uint64_t seed
     GenInjectParams Q;
     Q.g = make_gen_params(x, dt, n, seed, offset, dist, p0, p1);
     Q.y = (uint8_t *)y;
-    Q.m0 = (uint32_t)mseed;
-    Q.m1 = (uint32_t)(mseed >> 32);
     Q.mb0 = moff >> 2;
+    Q.mrk = round_keys(mseed);
     Q.T = T;
     Q.delta = delta;
     switch (dt) {

@@ -37,35 +37,48 @@ struct words4 {
     uint32_t v[4];
 };
 
-// Philox4x32-10 on counter (c0, c1, 0, 0) with key (k0, k1). Per round the
-// two 32x32->64 products M0*x0 and M1*x2 are formed and the state becomes
-// (hi(M1 x2) ^ x1 ^ k0, lo(M1 x2), hi(M0 x0) ^ x3 ^ k1, lo(M0 x0)); the key
-// advances by the Weyl constants between rounds. The key is wave-uniform,
-// so its schedule lives in scalar registers. Each three-way xor is one
-// gfx950 v_bitop3_b32 (truth table 0x96: odd parity of the three inputs).
-__device__ __forceinline__ words4 philox10(uint32_t c0, uint32_t c1, uint32_t k0, uint32_t k1)
+// The key schedule of one seed: round r uses (k0 + r 0x9E3779B9, k1 + r
+// 0xBB67AE85), mod 2^32. Computed once on the host and passed as kernel
+// arguments, so no wave spends scalar instructions rebuilding it.
+struct RoundKeys {
+    uint32_t k[20];
+};
+
+__host__ __device__ inline RoundKeys round_keys(uint64_t seed)
 {
-    uint32_t x0 = c0, x1 = c1, x2 = 0u, x3 = 0u;
+    RoundKeys r;
+    uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+    for (int i = 0; i < 10; ++i) {
+        r.k[2 * i] = k0;
+        r.k[2 * i + 1] = k1;
+        k0 += 0x9E3779B9u;
+        k1 += 0xBB67AE85u;
+    }
+    return r;
+}
+
+// Philox4x32-10 on counter (b mod 2^32, b >> 32, 0, 0) with the key schedule
+// rk. Per round the two 32x32->64 products M0*x0 and M1*x2 are formed and the
+// state becomes (hi(M1 x2) ^ x1 ^ k0, lo(M1 x2), hi(M0 x0) ^ x3 ^ k1,
+// lo(M0 x0)) with that round's key (k0, k1). The schedule is wave-uniform
+// and lives in scalar registers. Each three-way xor is one gfx950
+// v_bitop3_b32 (truth table 0x96: odd parity of the three inputs).
+__device__ __forceinline__ words4 philox_block(uint64_t b, const RoundKeys &rk)
+{
+    uint32_t x0 = (uint32_t)b, x1 = (uint32_t)(b >> 32), x2 = 0u, x3 = 0u;
 #pragma unroll
     for (int r = 0; r < 10; ++r) {
         const uint64_t p0 = (uint64_t)0xD2511F53u * (uint64_t)x0;
         const uint64_t p1 = (uint64_t)0xCD9E8D57u * (uint64_t)x2;
-        const uint32_t n0 = __builtin_amdgcn_bitop3_b32((uint32_t)(p1 >> 32), x1, k0, 0x96);
+        const uint32_t n0 = __builtin_amdgcn_bitop3_b32((uint32_t)(p1 >> 32), x1, rk.k[2 * r], 0x96);
         const uint32_t n1 = (uint32_t)p1;
-        const uint32_t n2 = __builtin_amdgcn_bitop3_b32((uint32_t)(p0 >> 32), x3, k1, 0x96);
+        const uint32_t n2 = __builtin_amdgcn_bitop3_b32((uint32_t)(p0 >> 32), x3, rk.k[2 * r + 1], 0x96);
         const uint32_t n3 = (uint32_t)p0;
         x0 = n0; x1 = n1; x2 = n2; x3 = n3;
-        k0 += 0x9E3779B9u;
-        k1 += 0xBB67AE85u;
     }
     words4 o;
     o.v[0] = x0; o.v[1] = x1; o.v[2] = x2; o.v[3] = x3;
     return o;
-}
-
-__device__ __forceinline__ words4 philox_block(uint64_t b, uint32_t k0, uint32_t k1)
-{
-    return philox10((uint32_t)b, (uint32_t)(b >> 32), k0, k1);
 }
 
 // ------------------------------------------------------- streaming memory

@@ -9,6 +9,14 @@
 // wave64 FMA per SIMD every 2 cycles. Only vector-register instructions appear
 // (plus VCC for the compare), and the one store is a guarded vector store.
 //
+// Three scalar instructions (the wave ballots' mask and count arithmetic and
+// the key-schedule adds) run the same way on eight SGPR chains: a CU's four
+// SIMDs share one scalar unit, so their cost per wave instruction per SIMD
+// is about four cycles. The last entry alternates one v_fma_f32 and one
+// s_add_u32 per chain step (eight of each per iteration): its cost per
+// v_fma_f32 shows whether the two units issue side by side (the scalar
+// chain's cost) or one after the other (their sum).
+//
 // Output: one JSON line {"reference": ..., "cycles": {instruction: cost},
 // "ms": {instruction: median kernel time}}.
 #include <hip/hip_runtime.h>
@@ -41,14 +49,15 @@ enum Op {
     FMA_F32, ADD_F32, MUL_F32, ADD_U32, AND_B32, LSHR_B32, BITOP3, FMAAK_F32,
     MAX_F32, MAX3_F32, CNDMASK, PERM, BFE, MUL_HI_U32, MAD_U64_U32,
     CVT_F32_U32, CVT_F32_F16, CVT_F32_FP8, CVT_PK_BF16_F32, CVT_PK_F16_F32,
-    CMP_F32, RCP_F32, SQRT_F32, CVT_PK_FP8_F32, NUM_OPS
+    CMP_F32, RCP_F32, SQRT_F32, CVT_PK_FP8_F32, S_ADD_U32, S_AND_B64, S_BCNT1_I32_B64, FMA_AND_SADD, NUM_OPS
 };
 
 static const char *kNames[NUM_OPS] = {
     "v_fma_f32", "v_add_f32", "v_mul_f32", "v_add_u32", "v_and_b32", "v_lshrrev_b32", "v_bitop3_b32", "v_fmaak_f32",
     "v_max_f32", "v_max3_f32", "v_cndmask_b32", "v_perm_b32", "v_bfe_u32", "v_mul_hi_u32", "v_mad_u64_u32",
     "v_cvt_f32_u32", "v_cvt_f32_f16", "v_cvt_f32_fp8", "v_cvt_pk_bf16_f32", "v_cvt_pk_f16_f32",
-    "v_cmp_lt_f32", "v_rcp_f32", "v_sqrt_f32", "v_cvt_pk_fp8_f32"};
+    "v_cmp_lt_f32", "v_rcp_f32", "v_sqrt_f32", "v_cvt_pk_fp8_f32", "s_add_u32", "s_and_b64", "s_bcnt1_i32_b64",
+    "v_fma_f32+s_add_u32"};
 
 template <int K>
 __global__ __launch_bounds__(kThreads) void k_rate(uint32_t *out, uint32_t seed)
@@ -100,6 +109,41 @@ __global__ __launch_bounds__(kThreads) void k_rate(uint32_t *out, uint32_t seed)
 #undef MAD
         }
         x0 = (uint32_t)(a0 ^ a1 ^ a2 ^ a3);
+    }
+    if constexpr (K == FMA_AND_SADD) {
+        uint32_t s0 = blockIdx.x + seed, s1 = s0 ^ 1u, s2 = s0 ^ 2u, s3 = s0 ^ 3u;
+        uint32_t s4 = s0 ^ 4u, s5 = s0 ^ 5u, s6 = s0 ^ 6u, s7 = s0 ^ 7u;
+#define V(v) asm volatile("v_fma_f32 %0, %0, %0, 1.0" : "+v"(v))
+#define S(v) asm volatile("s_add_u32 %0, %0, 1" : "+s"(v)::"scc")
+        for (int it = 0; it < kIter; ++it) {
+            V(x0); S(s0); V(x1); S(s1); V(x2); S(s2); V(x3); S(s3);
+            V(x4); S(s4); V(x5); S(s5); V(x6); S(s6); V(x7); S(s7);
+        }
+#undef V
+#undef S
+        x0 ^= s0 ^ s1 ^ s2 ^ s3 ^ s4 ^ s5 ^ s6 ^ s7;
+    }
+    if constexpr (K == S_ADD_U32 || K == S_AND_B64 || K == S_BCNT1_I32_B64) {
+        // wave-uniform chains in scalar registers
+        uint32_t s0 = blockIdx.x + seed, s1 = s0 ^ 1u, s2 = s0 ^ 2u, s3 = s0 ^ 3u;
+        uint32_t s4 = s0 ^ 4u, s5 = s0 ^ 5u, s6 = s0 ^ 6u, s7 = s0 ^ 7u;
+        uint64_t m0 = s0, m1 = s1, m2 = s2, m3 = s3;
+        for (int it = 0; it < kIter; ++it) {
+            if constexpr (K == S_ADD_U32) {
+#define S(v) asm volatile("s_add_u32 %0, %0, 1" : "+s"(v)::"scc")
+                S(s0); S(s1); S(s2); S(s3); S(s4); S(s5); S(s6); S(s7);
+#undef S
+            } else if constexpr (K == S_AND_B64) {
+#define S(m) asm volatile("s_and_b64 %0, %0, 0x7fffffff" : "+s"(m)::"scc")
+                S(m0); S(m1); S(m2); S(m3); S(m0); S(m1); S(m2); S(m3);
+#undef S
+            } else {
+#define S(d, m) asm volatile("s_bcnt1_i32_b64 %0, %1" : "=s"(d) : "s"(m) : "scc")
+                S(s0, m0); S(s1, m1); S(s2, m2); S(s3, m3); S(s4, m0); S(s5, m1); S(s6, m2); S(s7, m3);
+#undef S
+            }
+        }
+        x0 ^= s0 ^ s1 ^ s2 ^ s3 ^ s4 ^ s5 ^ s6 ^ s7 ^ (uint32_t)(m0 ^ m1 ^ m2 ^ m3);
     }
     const uint32_t r = x0 ^ x1 ^ x2 ^ x3 ^ x4 ^ x5 ^ x6 ^ x7;
     if (r == 0x9E3779B9u) out[0] = r;
