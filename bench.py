@@ -538,7 +538,10 @@ def main():
                                       warmup_ms=args.warmup_ms)), flush=True)
         return
     if args.kernels:
-        print(json.dumps(run_kernels()), flush=True)
+        out = run_kernels()
+        if args.calib_copy:
+            run_copy_calibration()
+        print(json.dumps(out), flush=True)
         return
     if args.configs:
         print(json.dumps(run_configs(not args.no_cpu_baseline)), flush=True)

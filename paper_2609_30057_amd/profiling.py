@@ -107,10 +107,35 @@ def cmd_stats(a):
         f.write("\n".join(lines) + "\n")
 
 
+def kernels_algo():
+    """Algorithmic bytes per launch of bench.py --kernels (N = 2^24): a
+    generator writes its elements, the injection reads x and writes y, the
+    fused generation with injection writes x and y, the two-operand check
+    reads both operands and the regenerated-reference check the candidate
+    only, the flush writes 1 GiB."""
+    N = 1 << 24
+    return {
+        "krex::k_gen<2, 0, true>": 16 * N * 2, "krex::k_gen<1, 1, false>": N * 2, "krex::k_gen<0, 1, false>": N * 4,
+        "krex::k_gen<0, 0, true>": 4 * N * 4, "krex::k_gen<3, 1, false>": 16 * N,
+        "krex::k_gen_packed<2, 0, 2>": 16 * N * 2, "krex::k_gen_packed<1, 1, 0>": N * 2,
+        "krex::k_gen_packed<3, 0, 2>": 16 * N, "krex::k_gen_packed<3, 1, 0>": 16 * N,
+        "krex::k_inject<2, 1>": 16 * N * 4, "krex::k_inject<3, 0>": 16 * N * 2, "krex::k_inject<0, 1>": 4 * N * 8,
+        "krex::k_gen_inject<2, 0, true, 1>": 16 * N * 4,
+        "krex::k_check<1, 0, true, 2>": N * 6, "krex::k_check<2, 2, true, 3>": 16 * N * 4,
+        "krex::k_check<3, 3, true, 3>": 16 * N * 2, "krex::k_check<0, 0, true, 2>": 4 * N * 8,
+        "krex::k_check_gen<2, 2, 0, true, true, 2>": 16 * N * 2, "krex::k_check_gen<3, 3, 1, false, true, 2>": 16 * N,
+        "krex::k_check_gen<0, 0, 0, true, true, 2>": 4 * N * 4, "krex::k_check_gen<1, 0, 1, false, true, 2>": N * 2,
+        "krex::k_flush": 1 << 30,
+    }
+
+
 def default_algo(workload):
-    """Algorithmic bytes per launch of the bench command's kernels: the
-    generation writes n elements, the check reads both operands (bf16
-    candidate, fp32 reference), the flush writes its buffer."""
+    """Algorithmic bytes per launch of the bench command's kernels (the
+    generation writes n elements, the check reads both operands, bf16
+    candidate and fp32 reference, the flush writes its buffer), or of
+    bench.py --kernels."""
+    if workload == "kernels":
+        return kernels_algo()
     if workload != "gemm_large":
         return {}
     from . import workloads as W
@@ -150,6 +175,8 @@ def cmd_traffic(a):
         cr = exact.get(ck)
         lines[-4] += (" The read-request counters by size give the copy %.1f MiB read (1024 expected)." % (cr / 2**20)
                       if cr else " The copy kernel is missing from the read-request pass.")
+    ours = [k for k in fetch if k.startswith(("krex", "void krex"))]
+    bases = [_short(k).split("::")[-1].split("<")[0] for k in ours]
     for k in sorted(fetch):
         if not k.startswith(("krex", "void krex")):
             continue
@@ -164,7 +191,10 @@ def cmd_traffic(a):
             "%.1f" % (al / 2**20) if al else "-", "%.3f" % ((rd + wb) / al) if al else "-"))
         fb = rd
         short = key.split("::")[-1].split("<")[0]
-        data["%s/%s" % (short, a.workload)] = {
+        # keyed by the kernel's name, or by its instantiation when the run
+        # holds several of one kernel
+        name = short if bases.count(short) == 1 else key.split("::")[-1]
+        data["%s/%s" % (name, a.workload)] = {
             "kernel": key, "hbm_bytes_per_launch": round(fb + wb), "fetch_bytes": round(fb), "write_bytes": round(wb),
             "algorithmic_bytes": al, "source_sha256": kernel_source_sha(short) if short in SECTION_OF else None}
     with open(a.out, "w") as f:
