@@ -8,8 +8,10 @@
 // [b 256 U, (b + 1) 256 U) of E elements (one 16-byte vector of the
 // narrower operand); thread t takes chunk b 256 U + u 256 + t for u < U, so
 // every step of a wave reads contiguous memory. Per element the verdict is
-// branch-free; mismatch and NaN counts are wave ballots summed on the scalar
-// unit; the per-lane maximum |a - b| is tracked per chunk, and the first
+// branch-free: each lane counts its mismatches in a vector register (summed
+// over the wave at the end), max_rel candidates are one wave ballot, and
+// unordered pairs are counted with ballots only in the rare chunks whose
+// maximum of d is NaN; the per-lane maximum |a - b| is tracked per chunk, and the first
 // index of the wave's maximum is recovered at the end by its winning lane
 // re-reading that one chunk. Each block writes one
 // 32-byte partial with plain stores; k_check_final reduces the partials and
@@ -54,7 +56,8 @@ struct CheckPartial {
 static_assert(sizeof(CheckPartial) == 32, "partial layout");
 
 struct LaneAcc {
-    uint32_t wmism, wnan;   // wave totals (exact in the wave's first lane)
+    uint32_t mism;          // this lane's mismatches
+    uint32_t wnan;          // the wave's unordered pairs (exact in its first lane)
     float rd, rb;           // element with the largest ratio d / |b| (rb = 0: +inf)
 };
 
@@ -84,8 +87,8 @@ __device__ __forceinline__ void ratio_update(float A, float B, LaneAcc &acc)
 // d >= kMinPositive.
 static constexpr float kMinPositive = 0x1p-149f;
 
-// Verdict of one element as wave ballots (each comparison lowers to one
-// compare writing a lane mask). d is 0 when a == b (an infinity equal to
+// Verdict of one element: the lane's mismatch count and the wave's max_rel
+// candidate mask (one compare writing a lane mask). d is 0 when a == b (an infinity equal to
 // itself included), NaN when the pair is unordered, else |a - b|. The
 // element mismatches exactly when not d <= min(atol + rtol |b|, FLT_MAX): an
 // equal pair has d = 0, below any threshold (atol, rtol >= 0; a NaN
@@ -97,19 +100,22 @@ static constexpr float kMinPositive = 0x1p-149f;
 // ratio may reach R (the filter's bound; R |b| is NaN only for an unordered
 // pair). NOINF: neither operand type has an infinity and their difference
 // cannot overflow (fp8 e4m3fn pairs: |a|, |b| <= 448), so |a - b| is already
-// 0 for equal operands and the threshold is finite: no select, no clamp.
-// Mismatches are counted here; unordered pairs are counted by the caller.
+// 0 for equal operands and the threshold is finite: no select, no clamp; and
+// the candidate test is fl(d Rup) > |b| with Rup >= (1/R)(1 + 2^-21) (see
+// RatioFilter), one product and one compare. Mismatches are counted here;
+// unordered pairs are counted by the caller.
 template <bool NOINF>
-__device__ __forceinline__ float elem_verdict(float A, float B, float rtol, float atol, float R, LaneAcc &acc,
-                                              uint64_t &cand)
+__device__ __forceinline__ float elem_verdict(float A, float B, float rtol, float atol, float R, float Rup,
+                                              LaneAcc &acc, uint64_t &cand)
 {
     const float d0 = __builtin_fabsf(A - B);
     const float ab = __builtin_fabsf(B);
     const float d = NOINF ? d0 : ((A == B) ? 0.0f : d0);
     const float rt = rtol * ab;
     const float thr = NOINF ? atol + rt : __builtin_fminf(atol + rt, 0x1.fffffep127f);
-    acc.wmism += popc(__ballot(!(d <= thr)));
-    cand |= __ballot(d >= __builtin_fmaxf(R * ab, kMinPositive));
+    acc.mism += (d <= thr) ? 0u : 1u;
+    if constexpr (NOINF) cand |= __ballot(d * Rup > ab);
+    else cand |= __ballot(d >= __builtin_fmaxf(R * ab, kMinPositive));
     return d;
 }
 
@@ -119,7 +125,7 @@ template <bool NOINF>
 __device__ __forceinline__ float check_elem(float A, float B, float rtol, float atol, LaneAcc &acc)
 {
     uint64_t cand = 0;
-    const float d = elem_verdict<NOINF>(A, B, rtol, atol, kRatioFloor, acc, cand);
+    const float d = elem_verdict<NOINF>(A, B, rtol, atol, kRatioFloor, 0.0f, acc, cand);
     acc.wnan += popc(__ballot(__builtin_isunordered(A, B)));
     ratio_update(A, B, acc);
     return d;
@@ -296,6 +302,13 @@ struct RefGen {
 template <int E>
 struct RatioFilter {
     float R = kRatioFloor;
+    // An upper bound of 1/R, at least (1/R)(1 + 2^-21): fl(1/R) (correctly
+    // rounded) times 1 + 2^-20. For fp8 pairs (|b| is 0 or at least 2^-9, d
+    // at most 896) an element with ratio d/|b| > R has d Rup > |b|(1 + 2^-21),
+    // at least four units in the last place of |b| above it (or above 0), so
+    // fl(d Rup) > |b|; an element with fl(d Rup) <= |b| therefore has ratio
+    // <= R, below the maximum, and is skipped. R = +inf gives Rup = 0.
+    float Rup = 0x1.00001p32f;
 
     __device__ __forceinline__ void chunk(const float (&A)[E], const float (&B)[E], bool valid, uint64_t cand,
                                           LaneAcc &acc)
@@ -311,6 +324,7 @@ struct RatioFilter {
         for (int off = 32; off > 0; off >>= 1) lo = __builtin_fmaxf(lo, __shfl_xor(lo, off, 64));
         lo = __uint_as_float(__builtin_amdgcn_readfirstlane(__float_as_uint(lo)));
         R = __builtin_fmaxf(R, lo);
+        Rup = (1.0f / R) * 0x1.00001p0f;
     }
 };
 
@@ -351,22 +365,29 @@ __device__ __forceinline__ void check_body(const uint8_t *a, const Ref &ref, uin
     uint32_t best_c = 0;                // its chunk
     constexpr bool NOINF = DA == F8 && DB == F8;
     // Counts and |a - b| maximum of one chunk; returns the lanes of the wave
-    // whose chunk has a max_rel candidate. Unordered pairs are rare: a sum
-    // of the chunk's d (non-negative, so NaN exactly when some pair is
-    // unordered) decides per wave whether to count them.
+    // whose chunk has a max_rel candidate. The chunk's maximum of d is taken
+    // with the NaN-propagating maximum, so it is NaN exactly when some pair
+    // is unordered (d is NaN only then); those rare chunks count their
+    // unordered pairs and take the maximum again without them.
     auto process = [&](const float (&A)[E], const float (&B)[E], uint64_t c) -> uint64_t {
-        float cmax = -1.0f;             // NaN d (unordered) is ignored by the maximum
-        float dsum = 0.0f;
+        float cmax = -1.0f;
         uint64_t cand = 0;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-            const float d = elem_verdict<NOINF>(A[e], B[e], rtol, atol, rf.R, acc, cand);
-            dsum += d;
-            cmax = __builtin_fmaxf(cmax, d);
+            const float d = elem_verdict<NOINF>(A[e], B[e], rtol, atol, rf.R, rf.Rup, acc, cand);
+            cmax = __builtin_elementwise_maximum(cmax, d);
         }
-        if (__ballot(dsum != dsum) != 0) {
+        // the counts are complete here: kept from being moved past the rare
+        // branch below, where their operands would need extra registers
+        __asm__ volatile("" : "+v"(acc.mism));
+        if (__ballot(cmax != cmax) != 0) {
 #pragma unroll
             for (int e = 0; e < E; ++e) acc.wnan += popc(__ballot(__builtin_isunordered(A[e], B[e])));
+            if (cmax != cmax) {
+                cmax = -1.0f;           // the maximum without the unordered pairs
+#pragma unroll
+                for (int e = 0; e < E; ++e) cmax = __builtin_fmaxf(cmax, elem_d(A[e], B[e]));
+            }
         }
         if (cmax > best_d) {
             best_d = cmax;
@@ -472,7 +493,10 @@ __device__ __forceinline__ void check_body(const uint8_t *a, const Ref &ref, uin
         const float r2 = __shfl_xor(rel, off, 64);
         rel = r2 > rel ? r2 : rel;
     }
-    const uint32_t wm = __shfl(acc.wmism, 0, 64), wn = __shfl(acc.wnan, 0, 64);
+    uint32_t wm = acc.mism;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) wm += __shfl_xor(wm, off, 64);
+    const uint32_t wn = __shfl(acc.wnan, 0, 64);
     __shared__ uint64_t s_key[kThreads / 64];
     __shared__ uint32_t s_m[kThreads / 64], s_n[kThreads / 64];
     __shared__ float s_r[kThreads / 64];
