@@ -575,6 +575,38 @@ __device__ __forceinline__ typename dtype_traits<DT>::storage perturb(typename d
     }
 }
 
+// The 4 G elements of s perturbed where their mask words (G Philox blocks)
+// are below T. At the commands' rates a perturbation is rare, so the
+// branches are wave-uniform (a ballot decides): one for the whole group,
+// then one per element, whose perturbation is computed for the wave and
+// selected per lane. Divergent per-lane branches would cost scalar
+// exec-mask instructions on every element.
+// T is in [0, 2^32]: w < T is tested as w <= T - 1 in 32 bits, T = 0 (no
+// element) returning at once.
+template <int DT, int MODE, int G>
+__device__ __forceinline__ void perturb_group(const words4 (&m)[G], uint64_t T, float delta,
+                                              typename dtype_traits<DT>::storage (&s)[4 * G])
+{
+    if (T == 0) return;
+    const uint32_t last = (uint32_t)(T - 1);
+    uint32_t wmin = m[0].v[0];     // the lane's smallest mask word (three-way minima)
+#pragma unroll
+    for (int i = 0; i < G; ++i)
+#pragma unroll
+        for (int l = 0; l < 4; ++l) wmin = wmin < m[i].v[l] ? wmin : m[i].v[l];
+    if (__ballot(wmin <= last) == 0) return;
+#pragma unroll
+    for (int i = 0; i < G; ++i)
+#pragma unroll
+        for (int l = 0; l < 4; ++l) {
+            const bool hit = m[i].v[l] <= last;
+            if (__ballot(hit) != 0) {
+                const typename dtype_traits<DT>::storage p = perturb<DT, MODE>(s[4 * i + l], delta);
+                s[4 * i + l] = hit ? p : s[4 * i + l];
+            }
+        }
+}
+
 template <int DT, int MODE>
 __global__ __launch_bounds__(kThreads) void k_inject(InjectParams P)
 {
@@ -588,13 +620,10 @@ __global__ __launch_bounds__(kThreads) void k_inject(InjectParams P)
     // The 4 G elements from the group starting at Philox block bfirst,
     // perturbed where their mask word is below T.
     auto mask_group = [&](uint64_t bfirst, Pack &pk) {
+        words4 m[G];
 #pragma unroll
-        for (int i = 0; i < G; ++i) {
-            const words4 w = philox_block(bfirst + i, P.rk);
-#pragma unroll
-            for (int l = 0; l < 4; ++l)
-                if ((uint64_t)w.v[l] < P.T) pk.s[4 * i + l] = perturb<DT, MODE>(pk.s[4 * i + l], P.delta);
-        }
+        for (int i = 0; i < G; ++i) m[i] = philox_block(bfirst + i, P.rk);
+        perturb_group<DT, MODE, G>(m, P.T, P.delta, pk.s);
     };
     const uint64_t gb0 = (uint64_t)blockIdx.x * P.U * kThreads;   // the block's first group
     const uint64_t gend = gb0 + (uint64_t)P.U * kThreads;
@@ -718,13 +747,10 @@ __global__ __launch_bounds__(kThreads) void k_gen_inject(GenInjectParams Q)
             transform4<DIST, POW2>(philox_block(bfirst + i, P.rk), P.p0, POW2 ? P.c : P.p1, v + 4 * i);
         pack_narrow<DT, DIST == BITCAST>(v, px.w);
         py.v = px.v;
+        words4 m[G];
 #pragma unroll
-        for (int i = 0; i < G; ++i) {
-            const words4 m = philox_block(mfirst + i, Q.mrk);
-#pragma unroll
-            for (int l = 0; l < 4; ++l)
-                if ((uint64_t)m.v[l] < Q.T) py.s[4 * i + l] = perturb<DT, MODE>(py.s[4 * i + l], Q.delta);
-        }
+        for (int i = 0; i < G; ++i) m[i] = philox_block(mfirst + i, Q.mrk);
+        perturb_group<DT, MODE, G>(m, Q.T, Q.delta, py.s);
     };
     // offset % 4 == 0 (the launcher guarantees it), so group g's first
     // element is 4 G g; blocks wholly in range store without per-lane checks.
