@@ -309,6 +309,10 @@ def run_kernels():
                                                                          sync=False)), xf.numel() * 4)
     rec("check_gen bf16 vs f32 normal 16.8M", t_ms(lambda: krex.check_gen(a_bf, torch.float32, 1, 1.6e-2, 1e-2,
                                                                            dist="normal", out=out, sync=False)), N * 2)
+    rec("check_gen_packed f16 vs f16 uniform 268M", t_ms(lambda: krex.check_gen_packed(
+        y16, torch.float16, 2, 1e-3, 1e-3, dist="uniform", p0=-4.0, p1=4.0, out=out, sync=False)), x16.numel() * 2)
+    rec("check_gen_packed f8 vs f8 uniform 268M", t_ms(lambda: krex.check_gen_packed(
+        y8, torch.float8_e4m3fn, 5, 0.125, 0.125, dist="uniform", p0=-4.0, p1=4.0, out=out, sync=False)), x8.numel())
     rec("flush 1GiB", t_ms(lambda: krex.flush(fl, 1)), GIB)
     return {"metric": "per-kernel throughput (algorithmic bytes / event time)", "unit": "GB/s",
             "peak_GBps": HBM_PEAK_GBPS, "kernels": res}

@@ -207,6 +207,17 @@ krex_status krex_check_gen(const void *a, int32_t dta, int32_t dtb, uint64_t n, 
                            int32_t dist, float p0, float p1, float rtol, float atol, krex_check_result *out,
                            void *stream);
 
+/* The same for the packed stream: *out equals krex_check(a, dta, b, dtb, n,
+ * rtol, atol) for the b that krex_gen_packed(b, dtb, n, seed, offset, dist,
+ * p0, p1) writes (offset in fields), regenerated in registers at one Philox
+ * block per 16 bytes of b (two for fp8 normal), so only a is read. Fastest
+ * when a is 16-byte aligned and offset is a multiple of 16 / size(dtb).
+ * Arguments and errors as for krex_gen_packed (dtb bf16, fp16 or fp8) and
+ * krex_check. */
+krex_status krex_check_gen_packed(const void *a, int32_t dta, int32_t dtb, uint64_t n, uint64_t seed,
+                                  uint64_t offset, int32_t dist, float p0, float p1, float rtol, float atol,
+                                  krex_check_result *out, void *stream);
+
 /* --- cache flush ------------------------------------------------------------
  * Writes `pattern` to every 32-bit word of buf[0..bytes) (device, 16-byte
  * aligned, bytes a multiple of 16) with stores that allocate in the

@@ -113,6 +113,7 @@ def lib():
             "krex_gen_inject": (i32, [vp, vp, i32, u64, u64, u64, i32, f32, f32, u64, u64, f64, f32, i32, vp]),
             "krex_check": (i32, [vp, i32, vp, i32, u64, f32, f32, vp, vp]),
             "krex_check_gen": (i32, [vp, i32, i32, u64, u64, u64, i32, f32, f32, f32, f32, vp, vp]),
+            "krex_check_gen_packed": (i32, [vp, i32, i32, u64, u64, u64, i32, f32, f32, f32, f32, vp, vp]),
             "krex_flush": (i32, [vp, u64, u32, vp]),
             "krex_probe": (i32, [u64, vp, vp]),
             "krex_region_begin": (i32, [vp, u32, vp, u64]),
@@ -293,6 +294,26 @@ def check_gen(a, dtype_b, seed, rtol, atol, offset=0, dist="uniform", p0=None, p
         out = check_result_buffer(a.device)
     _chk(lib().krex_check_gen(_dev(a), dtype_code(a.dtype), dtype_code(dtype_b), a.numel(), seed & (2**64 - 1), offset,
                               d, p0, p1, float(rtol), float(atol), _dev(out), _stream(stream)), "krex_check_gen")
+    if not sync:
+        return out
+    return decode_check_result(out)
+
+
+def check_gen_packed(a, dtype_b, seed, rtol, atol, offset=0, dist="uniform", p0=None, p1=None, out=None,
+                     stream=None, sync=True):
+    """check(a, b, rtol, atol) for the b that gen_packed(b, seed, offset,
+    dist, p0, p1) would write into a bf16 / fp16 / fp8 tensor of a's size,
+    regenerated instead of read (only a is read)."""
+    d = _dist(dist)
+    if p0 is None:
+        p0 = -1.0 if d == UNIFORM else 0.0
+    if p1 is None:
+        p1 = 1.0 if d == UNIFORM else (1.0 if d == NORMAL else 0.0)
+    if out is None:
+        out = check_result_buffer(a.device)
+    _chk(lib().krex_check_gen_packed(_dev(a), dtype_code(a.dtype), dtype_code(dtype_b), a.numel(),
+                                     seed & (2**64 - 1), offset, d, p0, p1, float(rtol), float(atol), _dev(out),
+                                     _stream(stream)), "krex_check_gen_packed")
     if not sync:
         return out
     return decode_check_result(out)

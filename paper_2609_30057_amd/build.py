@@ -2,9 +2,9 @@
 
   libkrexgate.so       the region coordinator (gate.cpp, plain POSIX C++),
                        one instance per process for both libraries below;
-  libkrex.so           the C ABI of include/krex.h: kernels.hip and
-                       check_gen.hip for gfx950 and api.cpp (host C++
-                       against the HIP runtime);
+  libkrex.so           the C ABI of include/krex.h: kernels.hip,
+                       check_gen.hip and check_gen_packed.hip for gfx950
+                       and api.cpp (host C++ against the HIP runtime);
   libkrex_intercept.so the ROCm tools library of include/krex_intercept.h
                        (loaded through HSA_TOOLS_LIB).
 
@@ -44,8 +44,8 @@ HOST = ["-x", "c++", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include"]
 # The HSA tools header includes its siblings by bare name under this macro.
 INTERCEPT = HOST + ["-DAMD_INTERNAL_BUILD", "-I/opt/rocm/include/hsa"]
 
-SOURCES = [("kernels.hip", DEVICE), ("check_gen.hip", DEVICE), ("api.cpp", HOST), ("gate.cpp", HOST),
-           ("intercept.cpp", INTERCEPT)]
+SOURCES = [("kernels.hip", DEVICE), ("check_gen.hip", DEVICE), ("check_gen_packed.hip", DEVICE), ("api.cpp", HOST),
+           ("gate.cpp", HOST), ("intercept.cpp", INTERCEPT)]
 
 
 def _compile(src, flags, verbose):
@@ -73,12 +73,13 @@ def _link(out, objs, extra, verbose, linker=HIPCC):
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        kernels, check_gen, api, gate, intercept = ex.map(lambda sf: _compile(sf[0], sf[1], verbose), SOURCES)
+        kernels, check_gen, check_gen_packed, api, gate, intercept = ex.map(
+            lambda sf: _compile(sf[0], sf[1], verbose), SOURCES)
     rpath = ["-L" + HERE, "-lkrexgate", "-Wl,-rpath,$ORIGIN", "-lpthread", "-lrt"]
     # The coordinator and the interceptor are plain host code: linked without
     # the HIP runtime (the interceptor loads inside the HSA runtime's start).
     _link(GATE_LIB, [gate], ["-Wl,-soname,libkrexgate.so", "-lpthread", "-lrt"], verbose, linker="g++")
-    _link(LIB, [kernels, check_gen, api], ["--offload-arch=" + ARCH, *rpath], verbose)
+    _link(LIB, [kernels, check_gen, check_gen_packed, api], ["--offload-arch=" + ARCH, *rpath], verbose)
     _link(INTERCEPT_LIB, [intercept], rpath, verbose, linker="g++")
     tmp = VALU_RATES + ".tmp%d" % os.getpid()
     cmd = [HIPCC, "-O3", "-std=c++17", "-x", "hip", "--offload-arch=" + ARCH, "-Xclang", "-target-feature",

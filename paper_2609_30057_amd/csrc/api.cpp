@@ -452,6 +452,29 @@ krex_status krex_check_gen(const void *a, int32_t dta, int32_t dtb, uint64_t n, 
     });
 }
 
+krex_status krex_check_gen_packed(const void *a, int32_t dta, int32_t dtb, uint64_t n, uint64_t seed,
+                                  uint64_t offset, int32_t dist, float p0, float p1, float rtol, float atol,
+                                  krex_check_result *out, void *stream)
+{
+    const size_t sa = elem_size(dta);
+    if (sa == 0 || dta == KREX_U32) return KREX_EINVAL;
+    if (dtb != KREX_BF16 && dtb != KREX_F16 && dtb != KREX_F8E4M3) return KREX_EINVAL;
+    if (!gen_params_ok(dist, p0, p1)) return KREX_EINVAL;
+    if (!(rtol >= 0.0f) || !(atol >= 0.0f) || !finite_f(rtol) || !finite_f(atol)) return KREX_EINVAL;
+    if (n >= (1ull << 33)) return KREX_EINVAL;
+    if (n > 0 && offset > UINT64_MAX - (n - 1)) return KREX_EINVAL;
+    if (!out) return KREX_EINVAL;
+    if (n > 0 && !a) return KREX_EINVAL;
+    if (!aligned(a, sa) || !aligned(out, 8)) return KREX_EALIGN;
+    hipStream_t s = (hipStream_t)stream;
+    void *scratch = nullptr;
+    const krex_status rc = check_scratch(s, &scratch);
+    if (rc != KREX_OK) return rc;
+    return submit(s, [&] {
+        return krex::launch_check_gen_packed(a, dta, dtb, n, seed, offset, dist, p0, p1, rtol, atol, scratch, out, s);
+    });
+}
+
 krex_status krex_flush(void *buf, uint64_t bytes, uint32_t pattern, void *stream)
 {
     if (bytes % 16 != 0) return KREX_EINVAL;

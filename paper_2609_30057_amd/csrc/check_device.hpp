@@ -299,6 +299,88 @@ struct RefGen {
 // every lane of the wave (the shuffles read
 // all lanes) with the wave's candidate mask; lanes without a chunk pass
 // valid = false.
+// Reference regenerated from the packed stream (krex_gen_packed): element i
+// is field offset + i, position (offset + i) mod EP of packed unit
+// (offset + i) / EP (EP = 16 / size of DB fields per unit), read back as
+// fp32. A chunk holds E / EP units' worth of fields; p0, p1 and rs are the
+// packed transform's constants and UM its uniform mode.
+template <int DB, int DIST, int UM, int E>
+struct RefGenPacked {
+    using TB = typename dtype_traits<DB>::storage;
+    static constexpr int SB = dtype_traits<DB>::size;
+    static constexpr int EP = packed_of<DB, DIST>::E;
+    static constexpr int NU = E / EP;        // units per chunk
+    static constexpr int NW = 4 * NU;        // words per chunk
+    static constexpr int PER = 4 / SB;       // fields per word
+    static_assert(E % EP == 0, "a chunk holds whole units");
+    struct Raw {};
+    uint64_t offset;    // field of element 0
+    RoundKeys rk;
+    float p0, p1, rs;
+
+    __device__ __forceinline__ static void widen_chunk(const uint32_t (&w)[NW], float (&B)[E])
+    {
+        union {
+            uint32_t w[NW];
+            TB s[E];
+        } u;
+#pragma unroll
+        for (int j = 0; j < NW; ++j) u.w[j] = w[j];
+        widen_words<DB, NW, E>(u.w, u.s, B);
+    }
+    __device__ __forceinline__ void load_raw(uint64_t, Raw &) const {}
+    // Chunk c when offset is a multiple of EP: NU whole units.
+    __device__ __forceinline__ void values(const Raw &, uint64_t c, float (&B)[E]) const
+    {
+        const uint64_t u0 = offset / EP + c * NU;
+        uint32_t w[NW];
+#pragma unroll
+        for (int k = 0; k < NU; ++k) {
+            uint32_t w4[4];
+            packed_unit<DB, DIST, UM>(u0 + k, rk, p0, p1, rs, w4);
+#pragma unroll
+            for (int l = 0; l < 4; ++l) w[4 * k + l] = w4[l];
+        }
+        widen_chunk(w, B);
+    }
+    // Any offset: the NU + 1 units the chunk's fields touch, shifted by
+    // s = offset mod EP fields (s / PER words, then a funnel shift of the
+    // rest; s is wave-uniform).
+    __device__ __forceinline__ void elems(uint64_t c, float (&B)[E]) const
+    {
+        const uint64_t u0 = (offset + c * E) / EP;
+        const uint32_t s = (uint32_t)(offset % EP);
+        uint32_t w[NW + 4];
+#pragma unroll
+        for (int k = 0; k < NU + 1; ++k) {
+            uint32_t w4[4];
+            packed_unit<DB, DIST, UM>(u0 + k, rk, p0, p1, rs, w4);
+#pragma unroll
+            for (int l = 0; l < 4; ++l) w[4 * k + l] = w4[l];
+        }
+        const uint32_t ws = s / PER, bs = (s % PER) * 8 * SB;
+        uint32_t o[NW];
+#pragma unroll
+        for (int j = 0; j < NW; ++j) {
+            const uint32_t lo = ws == 0 ? w[j] : ws == 1 ? w[j + 1] : ws == 2 ? w[j + 2] : w[j + 3];
+            const uint32_t hi = ws == 0 ? w[j + 1] : ws == 1 ? w[j + 2] : ws == 2 ? w[j + 3] : w[j + 4];
+            o[j] = __builtin_amdgcn_alignbit(hi, lo, bs);   // (hi:lo) >> bs, bs < 32
+        }
+        widen_chunk(o, B);
+    }
+    __device__ __forceinline__ float elem(uint64_t i) const
+    {
+        const uint64_t q = offset + i;
+        uint32_t w4[4];
+        packed_unit<DB, DIST, UM>(q / EP, rk, p0, p1, rs, w4);
+        const uint32_t k = (uint32_t)(q % EP);
+        const uint32_t wk = k / PER;
+        const uint32_t word = wk == 0 ? w4[0] : wk == 1 ? w4[1] : wk == 2 ? w4[2] : w4[3];
+        const uint32_t bits = (word >> (8 * SB * (k % PER))) & ((SB == 2) ? 0xFFFFu : 0xFFu);
+        return widen<DB>(bits);
+    }
+};
+
 template <int E>
 struct RatioFilter {
     float R = kRatioFloor;

@@ -233,23 +233,8 @@ hipError_t launch_gen(void *dst, int dt, uint64_t n, uint64_t seed, uint64_t off
 
 // ------------------------------------------------------------- packed stream
 //
-// The narrow-dtype generator that spends W bits of the word stream per
-// element (W = 16 for bf16 / fp16 and fp8 normal, 8 for fp8 uniform and
-// bitcast): field q is bits (q mod K) W .. of word q / K, K = 32 / W, low
-// bits first; element j uses field offset + j. One thread unit is one
-// 16-byte output vector, E elements = E fields = GB Philox blocks, so every
-// narrow dtype needs one block per 16 bytes (two for fp8 normal) instead of
-// one word per element. Uniform maps field f through the uniform transform
-// of the word f << (32 - W); normal runs Box-Muller on the two 16-bit fields
-// of one word widened to the top half (low field -> cosine, high field ->
-// sine); bitcast stores the fields, i.e. the words' bytes.
-
-template <int DT, int DIST>
-struct packed_of {
-    static constexpr int W = (DT == F8 && DIST != NORMAL) ? 8 : 16;
-    static constexpr int E = 16 / dtype_traits<DT>::size;
-    static constexpr int GB = E * W / 128;
-};
+// The generator of the packed stream (its units are built by packed_unit of
+// the device header): one thread unit is one 16-byte output vector.
 
 struct PackedParams {
     uint8_t *dst;
@@ -265,81 +250,19 @@ struct PackedParams {
     RoundKeys rk;      // the seed's Philox key schedule
 };
 
-// Uniform transform of a W-bit field f: UM_WORD applies the word-stream
-// transform to f << (32 - W); UM_SCALED when rs = fl(hi - lo) 2^-W is exact
-// (u = f 2^-W exactly, so rs f is the same real number as fl(hi - lo) u and
-// rounds the same: one conversion, one multiply, one add); UM_FUSED when rs f
-// is exact as well, so lo + rs f has one rounding: one fused multiply-add.
-enum : int { UM_WORD = 0, UM_SCALED = 1, UM_FUSED = 2 };
-
 template <int DT, int DIST, int UM>
 __global__ __launch_bounds__(kThreads) void k_gen_packed(PackedParams P)
 {
     using T = typename dtype_traits<DT>::storage;
     constexpr int ES = dtype_traits<DT>::size;
-    constexpr int W = packed_of<DT, DIST>::W;
-    constexpr int K = 32 / W;
     constexpr int E = packed_of<DT, DIST>::E;
-    constexpr int GB = packed_of<DT, DIST>::GB;
-    constexpr uint32_t kMask = (1u << W) - 1u;
     union Pack {
         uint4 v;
         uint32_t w[4];
         T s[E];
     };
-    // Unit u0 + g: GB Philox blocks, E fields transformed and packed into
-    // 16 bytes.
     auto unit_values = [&](uint64_t unit, Pack &pk) {
-        uint32_t wv[4 * GB];
-#pragma unroll
-        for (int i = 0; i < GB; ++i) {
-            const words4 w = philox_block(unit * GB + i, P.rk);
-#pragma unroll
-            for (int l = 0; l < 4; ++l) wv[4 * i + l] = w.v[l];
-        }
-        if constexpr (DIST == BITCAST) {
-            static_assert(GB == 1, "bitcast units are one block");
-#pragma unroll
-            for (int l = 0; l < 4; ++l) pk.w[l] = wv[l];
-        } else if constexpr (DIST == UNIFORM) {
-            float v[E];
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-                const uint32_t f = (wv[e / K] >> ((e % K) * W)) & kMask;
-                if constexpr (UM == UM_FUSED) {
-                    v[e] = __builtin_fmaf(P.rs, (float)f, P.p0);
-                } else if constexpr (UM == UM_SCALED) {
-                    const float t = P.rs * (float)f;
-                    v[e] = P.p0 + t;
-                } else {
-                    v[e] = uniform_f32(f << (32 - W), P.p0, P.p1);
-                }
-            }
-            if constexpr (DT == F8) {
-                // Two values per conversion (bytes 0-1, then 2-3 of the word).
-#pragma unroll
-                for (int i = 0; i < E / 4; ++i) {
-                    uint32_t wd = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(v[4 * i], v[4 * i + 1], 0, false);
-                    wd = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(v[4 * i + 2], v[4 * i + 3], (int)wd, true);
-                    pk.w[i] = wd;
-                }
-            } else {
-                pack_narrow<DT, false>(v, pk.w);
-            }
-        } else {
-            static_assert(W == 16 && E == 8 * GB, "normal fields are 16 bits, two per word");
-            float v[E];
-#pragma unroll
-            for (int i = 0; i < 4 * GB; ++i) {
-                float z0, z1;
-                normal_pair(wv[i] << 16, wv[i] & 0xFFFF0000u, z0, z1);
-                const float s0 = P.p1 * z0;
-                const float s1 = P.p1 * z1;
-                v[2 * i] = P.p0 + s0;
-                v[2 * i + 1] = P.p0 + s1;
-            }
-            pack_narrow<DT, false>(v, pk.w);
-        }
+        packed_unit<DT, DIST, UM>(unit, P.rk, P.p0, P.p1, P.rs, pk.w);
     };
     const uint64_t gb0 = (uint64_t)blockIdx.x * P.U * kThreads;   // the block's first unit (from u0)
     const uint64_t gend = gb0 + (uint64_t)P.U * kThreads;
@@ -376,18 +299,22 @@ __global__ __launch_bounds__(kThreads) void k_gen_packed(PackedParams P)
     }
 }
 
+int packed_transform_constants(int dt, int dist, float p0, float p1, float *q1, float *rs)
+{
+    const int W = (dt == F8 && dist != NORMAL) ? 8 : 16;
+    *q1 = (dist == UNIFORM) ? (p1 - p0) : p1;
+    *rs = 0.0f;
+    if (dist != UNIFORM) return UM_WORD;
+    *rs = ldexpf(*q1, -W);
+    if (ldexpf(*rs, W) != *q1) return UM_WORD;
+    float c;
+    return exact_scale(*q1, W, &c) ? UM_FUSED : UM_SCALED;
+}
+
 template <int DT, int DIST>
 static hipError_t gen_packed_dt_dist(PackedParams P, hipStream_t s)
 {
     constexpr int E = packed_of<DT, DIST>::E;
-    constexpr int W = packed_of<DT, DIST>::W;
-    P.umode = UM_WORD;
-    P.rs = 0.0f;
-    if (DIST == UNIFORM) {
-        P.rs = ldexpf(P.p1, -W);
-        float c;
-        if (ldexpf(P.rs, W) == P.p1) P.umode = exact_scale(P.p1, W, &c) ? UM_FUSED : UM_SCALED;
-    }
     P.u0 = P.offset / E;
     P.nunits = (P.offset + (P.n - 1)) / E - P.u0 + 1;
     P.vec = (P.offset % E == 0 && ((uintptr_t)P.dst & 15u) == 0) ? 1 : 0;
@@ -420,7 +347,7 @@ hipError_t launch_gen_packed(void *dst, int dt, uint64_t n, uint64_t seed, uint6
     P.offset = offset;
     P.rk = round_keys(seed);
     P.p0 = p0;
-    P.p1 = (dist == UNIFORM) ? (p1 - p0) : p1;
+    P.umode = packed_transform_constants(dt, dist, p0, p1, &P.p1, &P.rs);
     switch (dt) {
     case BF16: return gen_packed_dt<BF16>(P, dist, s);
     case F16: return gen_packed_dt<F16>(P, dist, s);

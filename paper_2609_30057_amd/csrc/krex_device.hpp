@@ -448,4 +448,97 @@ __device__ __forceinline__ void transform4(const words4 &w, float p0, float p1, 
     }
 }
 
+// ------------------------------------------------------------- packed stream
+//
+// The narrow-dtype stream that spends W bits of the word stream per
+// element (W = 16 for bf16 / fp16 and fp8 normal, 8 for fp8 uniform and
+// bitcast): field q is bits (q mod K) W .. of word q / K, K = 32 / W, low
+// bits first; element j uses field offset + j. One thread unit is one
+// 16-byte output vector, E elements = E fields = GB Philox blocks, so every
+// narrow dtype needs one block per 16 bytes (two for fp8 normal) instead of
+// one word per element. Uniform maps field f through the uniform transform
+// of the word f << (32 - W); normal runs Box-Muller on the two 16-bit fields
+// of one word widened to the top half (low field -> cosine, high field ->
+// sine); bitcast stores the fields, i.e. the words' bytes.
+
+template <int DT, int DIST>
+struct packed_of {
+    static constexpr int W = (DT == F8 && DIST != NORMAL) ? 8 : 16;
+    static constexpr int E = 16 / dtype_traits<DT>::size;
+    static constexpr int GB = E * W / 128;
+};
+
+// Uniform transform of a W-bit field f: UM_WORD applies the word-stream
+// transform to f << (32 - W); UM_SCALED when rs = fl(hi - lo) 2^-W is exact
+// (u = f 2^-W exactly, so rs f is the same real number as fl(hi - lo) u and
+// rounds the same: one conversion, one multiply, one add); UM_FUSED when rs f
+// is exact as well, so lo + rs f has one rounding: one fused multiply-add.
+enum : int { UM_WORD = 0, UM_SCALED = 1, UM_FUSED = 2 };
+
+// Packed unit `unit` of the stream with key schedule rk: its GB Philox
+// blocks (unit GB onward) give E = 16 / size fields, each transformed and
+// narrowed to DT, packed little-endian into the 16 bytes w. p0, p1: lo and
+// fl(hi - lo) (uniform) or mean and std (normal); rs: fl(hi - lo) 2^-W when
+// UM is UM_SCALED or UM_FUSED.
+template <int DT, int DIST, int UM>
+__device__ __forceinline__ void packed_unit(uint64_t unit, const RoundKeys &rk, float p0, float p1, float rs,
+                                            uint32_t (&w)[4])
+{
+    constexpr int W = packed_of<DT, DIST>::W;
+    constexpr int K = 32 / W;
+    constexpr int E = packed_of<DT, DIST>::E;
+    constexpr int GB = packed_of<DT, DIST>::GB;
+    constexpr uint32_t kMask = (1u << W) - 1u;
+    uint32_t wv[4 * GB];
+#pragma unroll
+    for (int i = 0; i < GB; ++i) {
+        const words4 blk = philox_block(unit * GB + i, rk);
+#pragma unroll
+        for (int l = 0; l < 4; ++l) wv[4 * i + l] = blk.v[l];
+    }
+    if constexpr (DIST == BITCAST) {
+        static_assert(GB == 1, "bitcast units are one block");
+#pragma unroll
+        for (int l = 0; l < 4; ++l) w[l] = wv[l];
+    } else if constexpr (DIST == UNIFORM) {
+        float v[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const uint32_t f = (wv[e / K] >> ((e % K) * W)) & kMask;
+            if constexpr (UM == UM_FUSED) {
+                v[e] = __builtin_fmaf(rs, (float)f, p0);
+            } else if constexpr (UM == UM_SCALED) {
+                const float t = rs * (float)f;
+                v[e] = p0 + t;
+            } else {
+                v[e] = uniform_f32(f << (32 - W), p0, p1);
+            }
+        }
+        if constexpr (DT == F8) {
+            // Two values per conversion (bytes 0-1, then 2-3 of the word).
+#pragma unroll
+            for (int i = 0; i < E / 4; ++i) {
+                uint32_t wd = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(v[4 * i], v[4 * i + 1], 0, false);
+                wd = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(v[4 * i + 2], v[4 * i + 3], (int)wd, true);
+                w[i] = wd;
+            }
+        } else {
+            pack_narrow<DT, false>(v, w);
+        }
+    } else {
+        static_assert(W == 16 && E == 8 * GB, "normal fields are 16 bits, two per word");
+        float v[E];
+#pragma unroll
+        for (int i = 0; i < 4 * GB; ++i) {
+            float z0, z1;
+            normal_pair(wv[i] << 16, wv[i] & 0xFFFF0000u, z0, z1);
+            const float s0 = p1 * z0;
+            const float s1 = p1 * z1;
+            v[2 * i] = p0 + s0;
+            v[2 * i + 1] = p0 + s1;
+        }
+        pack_narrow<DT, false>(v, w);
+    }
+}
+
 }  // namespace krex

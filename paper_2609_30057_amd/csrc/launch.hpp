@@ -22,6 +22,10 @@ bool gen_transform_constants(int dist, float p0, float p1, float *q1);
 // `p1` is the distribution's second parameter as given (upper bound or std).
 hipError_t launch_gen(void *dst, int dt, uint64_t n, uint64_t seed, uint64_t offset, int dist, float p0, float p1,
                       hipStream_t s);
+// The packed stream's transform constants for (dt, dist, p0, p1): *q1 the
+// range fl(p1 - p0) (uniform) or p1, *rs = *q1 2^-W (uniform); returns the
+// uniform mode (UM_WORD, UM_SCALED or UM_FUSED; UM_WORD otherwise).
+int packed_transform_constants(int dt, int dist, float p0, float p1, float *q1, float *rs);
 // Packed stream (bf16, fp16, fp8 only); offset counts fields.
 hipError_t launch_gen_packed(void *dst, int dt, uint64_t n, uint64_t seed, uint64_t offset, int dist, float p0,
                              float p1, hipStream_t s);
@@ -45,6 +49,11 @@ hipError_t launch_check(const void *a, int dta, const void *b, int dtb, uint64_t
 hipError_t launch_check_gen(const void *a, int dta, int dtb, uint64_t n, uint64_t seed, uint64_t offset, int dist,
                             float p0, float p1, float rtol, float atol, void *scratch, krex_check_result *out,
                             hipStream_t s);
+// As launch_check_gen for the reference krex_gen_packed would write
+// (dtb bf16, fp16 or fp8; offset counts fields).
+hipError_t launch_check_gen_packed(const void *a, int dta, int dtb, uint64_t n, uint64_t seed, uint64_t offset,
+                                   int dist, float p0, float p1, float rtol, float atol, void *scratch,
+                                   krex_check_result *out, hipStream_t s);
 hipError_t launch_flush(void *buf, uint64_t bytes, uint32_t pattern, hipStream_t s);
 hipError_t launch_probe(uint64_t iters, float *sink, hipStream_t s);
 hipError_t launch_sgemm(uint32_t M, uint32_t N, uint32_t K, const float *A, const float *B, float *C,

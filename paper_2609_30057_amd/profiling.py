@@ -125,6 +125,8 @@ def kernels_algo():
         "krex::k_check<3, 3, true, 3>": 16 * N * 2, "krex::k_check<0, 0, true, 2>": 4 * N * 8,
         "krex::k_check_gen<2, 2, 0, true, true, 2>": 16 * N * 2, "krex::k_check_gen<3, 3, 1, false, true, 2>": 16 * N,
         "krex::k_check_gen<0, 0, 0, true, true, 2>": 4 * N * 4, "krex::k_check_gen<1, 0, 1, false, true, 2>": N * 2,
+        "krex::k_check_gen_packed<2, 2, 0, 2, true, 2>": 16 * N * 2,
+        "krex::k_check_gen_packed<3, 3, 0, 2, true, 2>": 16 * N,
         "krex::k_flush": 1 << 30,
     }
 

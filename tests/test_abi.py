@@ -111,6 +111,13 @@ def test_host_only_entry_points():
                             None) == k.EALIGN
     assert L.krex_check_gen(ctypes.c_void_p(16), k.F32, k.F16, 4, 0, 0, 0, -1.0, 1.0, 0.0, 0.0, ctypes.c_void_p(12),
                             None) == k.EALIGN
+    # the packed-stream reference exists for the narrow dtypes only
+    assert L.krex_check_gen_packed(None, k.F32, k.F32, 4, 0, 0, 0, -1.0, 1.0, 0.0, 0.0, ctypes.c_void_p(8),
+                                   None) == k.EINVAL
+    assert L.krex_check_gen_packed(None, k.F32, k.F8E4M3, 4, 0, 0, 1, 0.0, -1.0, 0.0, 0.0, ctypes.c_void_p(8),
+                                   None) == k.EINVAL
+    assert L.krex_check_gen_packed(ctypes.c_void_p(2), k.F32, k.BF16, 4, 0, 0, 0, -1.0, 1.0, 0.0, 0.0,
+                                   ctypes.c_void_p(8), None) == k.EALIGN
     assert L.krex_inject(None, None, k.F16, 4, 0, 0, 1.5, 0.5, 1, None) == k.EINVAL
     assert L.krex_flush(None, 17, 0, None) == k.EINVAL
     assert L.krex_region_begin(None, 10, None, 0) == k.ENOTATTACHED
