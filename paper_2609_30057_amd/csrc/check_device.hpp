@@ -1,7 +1,8 @@
 // check_device.hpp -- the fused allclose check (Section 1; Section 2.1: the
 // command checks the candidate's output against a reference) as a device
-// body shared by its two kernels: k_check reads the reference operand from
-// memory, k_check_gen regenerates it from its Philox stream (the values
+// body shared by its kernels, which differ in where the reference comes
+// from: k_check reads it from memory, k_check_gen and k_check_gen_packed
+// regenerate it from the word or the packed Philox stream (the values
 // generation would have written), so only the candidate is read.
 //
 // Two launches and no atomics. k_check: block b owns chunks
@@ -11,11 +12,11 @@
 // branch-free: each lane counts its mismatches in a vector register (summed
 // over the wave at the end), max_rel candidates are one wave ballot, and
 // unordered pairs are counted with ballots only in the rare chunks whose
-// maximum of d is NaN; the per-lane maximum |a - b| is tracked per chunk, and the first
-// index of the wave's maximum is recovered at the end by its winning lane
-// re-reading that one chunk. Each block writes one
-// 32-byte partial with plain stores; k_check_final reduces the partials and
-// writes the result record.
+// maximum of d is NaN. The per-lane maximum |a - b| is tracked per chunk,
+// and the first index of the wave's maximum is recovered at the end by its
+// winning lane re-reading that one chunk. Each block writes one 32-byte
+// partial with plain stores; k_check_final reduces the partials and writes
+// the result record.
 //
 // max_rel without a division per element: a lane keeps the pair (d*, b*)
 // with the largest exact ratio d / |b| among its elements with finite
@@ -88,8 +89,9 @@ __device__ __forceinline__ void ratio_update(float A, float B, LaneAcc &acc)
 static constexpr float kMinPositive = 0x1p-149f;
 
 // Verdict of one element: the lane's mismatch count and the wave's max_rel
-// candidate mask (one compare writing a lane mask). d is 0 when a == b (an infinity equal to
-// itself included), NaN when the pair is unordered, else |a - b|. The
+// candidate mask (one compare writing a lane mask). d is 0 when a == b (an
+// infinity equal to itself included), NaN when the pair is unordered, else
+// |a - b|. The
 // element mismatches exactly when not d <= min(atol + rtol |b|, FLT_MAX): an
 // equal pair has d = 0, below any threshold (atol, rtol >= 0; a NaN
 // threshold, 0 x inf with |b| = inf, becomes FLT_MAX); an unordered pair has
