@@ -533,7 +533,7 @@ def main():
     ap.add_argument("--valu-rates", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (use --gpus 1)", file=sys.stderr)
+        print("bench.py measures one GPU: the library has no multi-GPU path (use --gpus 1)", file=sys.stderr)
         sys.exit(2)
     if args.fidelity:
         from paper_2609_30057_amd import fidelity
