@@ -352,7 +352,7 @@ def configs_cpu_baseline(cmds):
     tg, x = t(lambda: oracle.gen("f16", m, cfg["seed"], 0, 0, cfg["p0"], cfg["p1"]))
     ti, (y, _) = t(lambda: oracle.inject(x, "f16", cfg["mask_seed"], cfg["rate"], cfg["delta"], oracle.INJ_EXACT))
     tc, _ = t(lambda: oracle.check(y, "f16", x, "f16", cfg["rtol"], cfg["atol"]))
-    out["check_stress"] = {"value": round(m * 10 / (tg + ti + tc) / 1e9, 3), "unit": "GB/s", "cores": 1,
+    out["check_stress"] = {"value": round(m * 8 / (tg + ti + tc) / 1e9, 3), "unit": "GB/s", "cores": 1,
                            "kind": "oracle", "sample": "the first eighth of the rows (33,554,432 elements): "
                            "generation %.2f s, injection %.2f s, check %.2f s" % (tg, ti, tc)}
     cfg = W.MIXED_STREAM
@@ -364,7 +364,7 @@ def configs_cpu_baseline(cmds):
         ti, (y, _) = t(lambda: oracle.inject(x, dtn, c.mask_seed, c.rate, cfg["delta"], oracle.INJ_ROUND))
         tc, _ = t(lambda: oracle.check(y, dtn, x, dtn, c.rtol, c.atol))
         secs += tg + ti + tc
-        total += c.nbytes * 5
+        total += c.nbytes * 4
     secs += flush_s(cfg["flush_bytes"], len(sample), 2)
     total += len(sample) * cfg["flush_bytes"]
     out["mixed_stream"] = {"value": round(total / secs / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
@@ -378,7 +378,12 @@ def run_configs(with_cpu=True):
     512 MiB flush in a region), check_stress (gen + inject + check of 256M
     fp16), mixed_stream (64 derived commands: gen, inject, check with the
     verdict read back, 512 MiB flush). GB/s = algorithmic bytes / summed
-    event time of the hot-path kernels; mixed_stream also reports wall
+    event time of the hot-path kernels, the bytes as the method defines
+    them: generation and injection each write n elements (injection's read
+    of x is not counted, x could be regenerated), the check reads both
+    operands, the flush writes its buffer. The per-kernel rates beside them
+    (gen_GBps, inject_GBps, check_GBps) count the bytes each kernel moves
+    (injection: x read and y written). mixed_stream also reports wall
     commands/s including launches and verdict readback."""
     import numpy as np
     import torch
@@ -441,9 +446,9 @@ def run_configs(with_cpu=True):
         e3 = ev()
         v = krex.decode_check_result(res)
     tg, ti, tc = e0.elapsed_time(e1), e1.elapsed_time(e2), e2.elapsed_time(e3)
-    nbytes = m * 2 + m * 4 + m * 4
+    nbytes = m * 2 + m * 2 + m * 4
     # the same command with generation and injection fused (x and y written
-    # in one pass, x not read back): 8 bytes per element instead of 10
+    # in one pass, x not read back): 8 bytes per element moved instead of 10
     for _ in range(2):
         f0 = ev()
         krex.gen_inject(x, y, cfg["seed"], 0, "uniform", cfg["p0"], cfg["p1"], mask_seed=cfg["mask_seed"],
@@ -489,7 +494,7 @@ def run_configs(with_cpu=True):
         e1 = ev()
         krex.decode_check_result(res)
         kernel_ms += e0.elapsed_time(e1)
-        total += c.nbytes * 5 + cfg["flush_bytes"]
+        total += c.nbytes * 4 + cfg["flush_bytes"]
     wall = time.perf_counter() - t0
     out["commands"]["mixed_stream"] = {"GBps": round(total / (kernel_ms / 1e3) / 1e9, 1), "bytes": total,
                                        "wall_GBps": round(total / wall / 1e9, 1),
