@@ -376,8 +376,8 @@ def configs_cpu_baseline(cmds):
 def run_configs(with_cpu=True):
     """The other commands end to end: gemm_tiny (gen + check + 100 reps with a
     512 MiB flush in a region), check_stress (gen + inject + check of 256M
-    fp16), mixed_stream (64 derived commands: gen, inject, check with the
-    verdict read back, 512 MiB flush). GB/s = algorithmic bytes / summed
+    fp16), mixed_stream (64 derived commands: gen and inject in one call,
+    check with the verdict read back, 512 MiB flush). GB/s = algorithmic bytes / summed
     event time of the hot-path kernels, the bytes as the method defines
     them: generation and injection each write n elements (injection's read
     of x is not counted, x could be regenerated), the check reads both
@@ -487,8 +487,9 @@ def run_configs(with_cpu=True):
         xv = xbuf[:c.nbytes].view(tdt[c.dtype])
         yv = ybuf[:c.nbytes].view(tdt[c.dtype])
         e0 = ev()
-        krex.gen(xv, c.value_seed, 0, c.dist, c.p0, c.p1)
-        krex.inject(yv, xv, c.mask_seed, c.rate, cfg["delta"], "round")
+        # x and y in one pass (the same tensors as generation, then injection)
+        krex.gen_inject(xv, yv, c.value_seed, 0, c.dist, c.p0, c.p1, mask_seed=c.mask_seed, rate=c.rate,
+                        delta=cfg["delta"], mode="round")
         krex.check(yv, xv, c.rtol, c.atol, out=res, sync=False)
         krex.flush(fl512)
         e1 = ev()
