@@ -4,7 +4,8 @@ all 16 dtype pairs, uniform (power-of-two and other ranges), normal and
 bitcast references, ragged sizes, word offsets that are multiples of 4 (the
 vector path) and ones that are not, a misaligned candidate, n = 0; then
 equality with the two-operand GPU check at 2^24 + 7 elements and on the
-check-stress command's full 268,435,456 fp16 elements."""
+check-stress command's full 268,435,456 fp16 elements, and exact records at
+the largest n, 2^33 - 1."""
 import pytest
 import torch
 
@@ -117,3 +118,34 @@ def test_check_gen_rejects_bad_arguments():
         krex.check_gen(a, torch.int32, 1, 0.0, 0.0)
     with pytest.raises(krex.KrexError):
         krex.check_gen(a, torch.float16, 1, 0.0, 0.0, offset=2**64 - 8)
+
+
+def _plant(a, idx, byte):
+    """Sets fp8 element i of a to the bit pattern `byte`; returns the
+    values before and after (exact fp32)."""
+    v = a.view(torch.uint8)
+    before = [float(a[i].float().item()) for i in idx]
+    for i in idx:
+        v[i] = byte
+    after = [float(a[i].float().item()) for i in idx]
+    return before, after
+
+
+def test_check_gen_at_the_largest_n():
+    """n = 2^33 - 1 fp8 elements against the regenerated reference: zero
+    record for the generated tensor itself, then three planted changes on
+    both sides of index 2^32 and in the n mod 16 tail give the exact
+    record."""
+    n = 2**33 - 1
+    a = torch.empty(n, dtype=torch.float8_e4m3fn, device="cuda")
+    krex.gen(a, 71, 0, "uniform", -4.0, 4.0)
+    r = krex.check_gen(a, torch.float8_e4m3fn, 71, 0.0, 0.0, dist="uniform", p0=-4.0, p1=4.0)
+    assert (r.n, r.mismatches, r.nan_count, r.max_abs, r.argmax_abs, r.max_rel) == (n, 0, 0, 0.0, 0, 0.0)
+    idx = [5, 2**32 + 9, n - 1]
+    before, after = _plant(a, idx, 0x58)              # 0x58 = 16.0, outside [-4, 4]
+    r = krex.check_gen(a, torch.float8_e4m3fn, 71, 0.0, 0.0, dist="uniform", p0=-4.0, p1=4.0)
+    d = [abs(x - y) for x, y in zip(after, before)]
+    assert r.mismatches == 3 and r.nan_count == 0
+    assert r.max_abs == max(d) and r.argmax_abs == idx[d.index(max(d))]
+    del a
+    torch.cuda.empty_cache()

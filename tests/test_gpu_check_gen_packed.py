@@ -6,7 +6,7 @@ three uniform modes (fused multiply-add, scaled, word transform), normal and
 bitcast; ragged sizes; offsets that are multiples of a unit (the vector
 path) and ones that are not (the shifted element path); a misaligned
 candidate; then equality with the two-operand GPU check at 2^24 + 7
-elements."""
+elements, and exact records at the largest n, 2^33 - 1."""
 import pytest
 import torch
 
@@ -92,3 +92,26 @@ def test_check_gen_packed_empty_and_rejections():
         krex.check_gen_packed(a, torch.float16, 1, 0.0, 0.0, dist="normal", p0=0.0, p1=-1.0)
     with pytest.raises(krex.KrexError):
         krex.check_gen_packed(a, torch.float16, 1, float("inf"), 0.0)
+
+
+def test_check_gen_packed_at_the_largest_n():
+    """n = 2^33 - 1 fp8 elements against the regenerated packed reference:
+    zero record for the generated tensor itself, then planted changes on
+    both sides of index 2^32 and in the tail give the exact record."""
+    n = 2**33 - 1
+    a = torch.empty(n, dtype=torch.float8_e4m3fn, device="cuda")
+    krex.gen_packed(a, 81, 0, "uniform", -4.0, 4.0)
+    r = krex.check_gen_packed(a, torch.float8_e4m3fn, 81, 0.0, 0.0, dist="uniform", p0=-4.0, p1=4.0)
+    assert (r.n, r.mismatches, r.nan_count, r.max_abs, r.argmax_abs, r.max_rel) == (n, 0, 0, 0.0, 0, 0.0)
+    idx = [7, 2**32 + 3, n - 2]
+    v = a.view(torch.uint8)
+    before = [float(a[i].float().item()) for i in idx]
+    for i in idx:
+        v[i] = 0xD8                                    # -16.0
+    after = [float(a[i].float().item()) for i in idx]
+    r = krex.check_gen_packed(a, torch.float8_e4m3fn, 81, 0.0, 0.0, dist="uniform", p0=-4.0, p1=4.0)
+    d = [abs(x - y) for x, y in zip(after, before)]
+    assert r.mismatches == 3 and r.nan_count == 0
+    assert r.max_abs == max(d) and r.argmax_abs == idx[d.index(max(d))]
+    del a
+    torch.cuda.empty_cache()
