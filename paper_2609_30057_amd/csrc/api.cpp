@@ -129,7 +129,7 @@ private:
     {
         std::lock_guard<std::mutex> g(pool_mu_);
         if (dev >= 0 && dev < 64) pool_[dev].push_back(ev);
-        else hipEventDestroy(ev);
+        else (void)hipEventDestroy(ev);   // a pool beyond 64 devices is not kept
     }
 
     void run()
@@ -145,7 +145,8 @@ private:
                 q_.pop_front();
             }
             if (it.dev != cur) {
-                hipSetDevice(it.dev);
+                // a failure shows in the event wait below, which marks the slot failed
+                (void)hipSetDevice(it.dev);
                 cur = it.dev;
             }
             // A failed wait means the context hit a device error: the count is

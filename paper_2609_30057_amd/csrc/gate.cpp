@@ -177,7 +177,7 @@ int children_of(int32_t pid, int32_t *out, int max)
     int n = 0;
     while (dirent *e = readdir(d)) {
         if (e->d_name[0] < '0' || e->d_name[0] > '9') continue;
-        char cp[96];
+        char cp[sizeof "/proc//task//children" + 12 + sizeof e->d_name];
         snprintf(cp, sizeof cp, "/proc/%d/task/%s/children", (int)pid, e->d_name);
         FILE *f = fopen(cp, "r");
         if (!f) continue;
