@@ -122,8 +122,7 @@ __global__ __launch_bounds__(kThreads) void k_gen(GenParams P)
 }
 
 // Units per thread and grid of the block-contiguous layout: block b owns
-// units [b 256 U, (b + 1) 256 U). One unit per thread (a one-shot grid in
-// address order) streams HBM fastest on gfx950; U grows only to keep a
+// units [b 256 U, (b + 1) 256 U). U grows beyond u_pref only to keep a
 // dispatch within 2^31 work-items.
 static void shape(uint64_t units, uint32_t u_pref, uint32_t *U, uint32_t *grid)
 {
@@ -167,10 +166,41 @@ bool gen_transform_constants(int dist, float p0, float p1, float *q1)
     return false;
 }
 
+// Preferred units per thread, measured per kernel on gfx950 (rocprofv3
+// averages at 268M narrow / 67M fp32 elements). One unit per thread, a
+// one-shot grid in address order, streams HBM fastest: it wins where the
+// stores bound the kernel (fp32 and packed 16-bit uniform generation, fp32
+// and 16-bit injection) and, less clearly, for the normal transform. Where a
+// unit's Philox work takes about as long as its store (narrow word-stream
+// uniform and bitcast generation, the packed fp8 uniform stream, fp8
+// injection and narrow generation with injection), four units per thread
+// are 5-10% faster: a wave's store of one unit overlaps its arithmetic for
+// the next, and a quarter of the waves are dispatched. The packed normal
+// transform gains ~4% from two. KREX_GEN_U, KREX_PACKED_U, KREX_INJECT_U and
+// KREX_GEN_INJECT_U override these.
+template <int DT, int DIST>
+static constexpr uint32_t gen_units()
+{
+    return (DIST != NORMAL && dtype_traits<DT>::size <= 2) ? 4u : 1u;
+}
+
+template <int DT, int DIST>
+static constexpr uint32_t packed_units()
+{
+    return DIST == NORMAL ? 2u : (DT == F8 && DIST == UNIFORM) ? 4u : 1u;
+}
+
+template <int DT>
+static constexpr uint32_t inject_units()
+{
+    return dtype_traits<DT>::size == 1 ? 4u : 1u;
+}
+
 template <int DT, int DIST>
 static hipError_t gen_dt_dist(GenParams P, hipStream_t s)
 {
-    static const uint32_t u_pref = tune_env("KREX_GEN_U", 1);
+    static const uint32_t u_env = tune_env("KREX_GEN_U", 0);
+    const uint32_t u_pref = u_env ? u_env : gen_units<DT, DIST>();
     uint32_t grid;
     shape(P.ngroups, u_pref, &P.U, &grid);
     if constexpr (DIST == UNIFORM && DT != U32)
@@ -318,8 +348,10 @@ static hipError_t gen_packed_dt_dist(PackedParams P, hipStream_t s)
     P.u0 = P.offset / E;
     P.nunits = (P.offset + (P.n - 1)) / E - P.u0 + 1;
     P.vec = (P.offset % E == 0 && ((uintptr_t)P.dst & 15u) == 0) ? 1 : 0;
+    static const uint32_t u_env = tune_env("KREX_PACKED_U", 0);
+    const uint32_t u_pref = u_env ? u_env : packed_units<DT, DIST>();
     uint32_t grid;
-    shape(P.nunits, 1, &P.U, &grid);
+    shape(P.nunits, u_pref, &P.U, &grid);
     if constexpr (DIST == UNIFORM) {
         if (P.umode == UM_FUSED) return launch(k_gen_packed<DT, DIST, UM_FUSED>, dim3(grid), dim3(kThreads), s, P);
         if (P.umode == UM_SCALED) return launch(k_gen_packed<DT, DIST, UM_SCALED>, dim3(grid), dim3(kThreads), s, P);
@@ -599,7 +631,8 @@ __global__ __launch_bounds__(kThreads) void k_inject(InjectParams P)
 template <int DT>
 static hipError_t inject_dt(InjectParams P, int mode, hipStream_t s)
 {
-    static const uint32_t u_pref = tune_env("KREX_INJECT_U", 1);
+    static const uint32_t u_env = tune_env("KREX_INJECT_U", 0);
+    const uint32_t u_pref = u_env ? u_env : inject_units<DT>();
     uint32_t grid;
     shape(P.ngroups, u_pref, &P.U, &grid);
     if (mode == INJ_ROUND) return launch(k_inject<DT, INJ_ROUND>, dim3(grid), dim3(kThreads), s, P);
@@ -717,8 +750,10 @@ __global__ __launch_bounds__(kThreads) void k_gen_inject(GenInjectParams Q)
 template <int DT, int DIST, bool POW2>
 static hipError_t gen_inject_mode(GenInjectParams Q, int mode, hipStream_t s)
 {
+    static const uint32_t u_env = tune_env("KREX_GEN_INJECT_U", 0);
+    const uint32_t u_pref = u_env ? u_env : gen_units<DT, DIST>();
     uint32_t grid;
-    shape(Q.g.ngroups, 1, &Q.g.U, &grid);
+    shape(Q.g.ngroups, u_pref, &Q.g.U, &grid);
     if (mode == INJ_ROUND) return launch(k_gen_inject<DT, DIST, POW2, INJ_ROUND>, dim3(grid), dim3(kThreads), s, Q);
     return launch(k_gen_inject<DT, DIST, POW2, INJ_EXACT>, dim3(grid), dim3(kThreads), s, Q);
 }

@@ -254,14 +254,16 @@ def cmd_valu_model(a):
         grid = int(r.get("Grid_Size") or r["Grid_Size_X"])
         launches.setdefault(name, []).append((grid, dur))
     clock = 2.4e9
+    algo = kernels_algo()
     lines = ["# Vector-issue roofline of the generation kernels: %s" % a.title, "",
              "Commands (from the repository root):", "", "    " + a.cmd.replace(" ;; ", "\n    "), "",
              "Per unit (one thread, one 16-byte output vector) the kernel runs the vector instructions of its "
-             "unit path; each costs its measured issue cycles per wave64 instruction (v_fma_f32 = 2). The launch "
-             "needs waves x weighted cycles / (4 SIMDs x %d CUs x 2.4 GHz) at full vector issue." % a.cus, "",
-             "Each unit also writes one 16-byte vector: grid x 16 bytes at 8 TB/s is the launch's HBM time. The "
+             "unit path; each costs its measured issue cycles per wave64 instruction (v_fma_f32 = 2). A launch "
+             "of u units (its output bytes / 16; a thread may take several) needs u / 64 unit-waves x weighted "
+             "cycles / (4 SIMDs x %d CUs x 2.4 GHz) at full vector issue." % a.cus, "",
+             "Each unit also writes one 16-byte vector: u x 16 bytes at 8 TB/s is the launch's HBM time. The "
              "larger of the two times bounds the kernel.", "",
-             "| Kernel | Vector instr. per unit | Weighted cycles per wave | Waves | Time at full issue (us) "
+             "| Kernel | Vector instr. per unit | Weighted cycles per unit-wave | Unit-waves | Time at full issue (us) "
              "| HBM time (us) | Bound | Measured (us) | Fraction of the bound |", "|---|---|---|---|---|---|---|---|---|"]
     for name in sorted(launches):
         args = re.match(r"krex::k_gen(?:_packed)?<(.*)>", name).group(1).split(", ")
@@ -274,9 +276,10 @@ def cmd_valu_model(a):
         grid, _ = max(launches[name])
         durs = [d for g, d in launches[name] if g == grid]
         meas = statistics.median(durs)
-        waves = grid / 64.0
+        units = algo[name] / 16 if name in algo else grid
+        waves = units / 64.0
         t = waves * cyc / (4 * a.cus * clock) * 1e6
-        th = grid * 16 / 8e12 * 1e6
+        th = units * 16 / 8e12 * 1e6
         lines.append("| `%s` | %d | %.0f | %d | %.1f | %.1f | %s | %.1f | %.2f |" % (
             name, len(ops), cyc, waves, t, th, "issue" if t >= th else "HBM", meas, max(t, th) / meas))
     with open(a.out, "w") as f:
