@@ -951,7 +951,7 @@ hipError_t launch_check(const void *a, int dta, const void *b, int dtb, uint64_t
 // persistent grid-stride loops (whose 2048 concurrently active blocks spread
 // each wave of stores across the whole buffer).
 //
-// The stores (store16_stream, raw buffer stores) carry the system-scope
+// The stores (store16_alloc, raw buffer stores) carry the system-scope
 // coherence bits (sc0 sc1): they write through L2 without allocating there,
 // which streams ~2% faster, and still
 // allocate in the Infinity Cache, whose contents the flush exists to evict
@@ -963,8 +963,8 @@ hipError_t launch_check(const void *a, int dta, const void *b, int dtb, uint64_t
 __global__ __launch_bounds__(kThreads) void k_flush(uint4 *buf, uint64_t nvec, uint32_t pattern)
 {
     const uint64_t i = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (i < nvec) store16_stream(buf + (uint64_t)blockIdx.x * kThreads, 16u * threadIdx.x,
-                                 make_uint4(pattern, pattern, pattern, pattern));
+    if (i < nvec) store16_alloc(buf + (uint64_t)blockIdx.x * kThreads, 16u * threadIdx.x,
+                                make_uint4(pattern, pattern, pattern, pattern));
 }
 
 hipError_t launch_flush(void *buf, uint64_t bytes, uint32_t pattern, hipStream_t s)

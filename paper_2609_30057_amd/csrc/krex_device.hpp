@@ -94,22 +94,41 @@ __device__ __forceinline__ uint4 load16_stream(const void *p)
     return make_uint4(v.x, v.y, v.z, v.w);
 }
 
-// 16-byte store of a generated output with the system-scope coherence bits
-// (sc0 sc1): written through L2 without allocating there (L2 does not carry
-// data from one launch to the next on this GPU anyway) and allocated in the
-// Infinity Cache like an ordinary store, ~2% faster for streamed writes. It
-// is a raw buffer store, so the compiler sees it and keeps the wait states a
-// store needs before its data registers are overwritten. `base` must be the
-// same for every lane of the wave (a block's first byte); `off` is the
-// lane's byte offset from it, below 2^31.
-__device__ __forceinline__ void store16_stream(void *base, uint32_t off, const uint4 &u)
+// 16-byte raw buffer store with cache-policy bits POL. A raw buffer store,
+// so the compiler sees it and keeps the wait states a store needs before its
+// data registers are overwritten. `base` must be the same for every lane of
+// the wave (a block's first byte); `off` is the lane's byte offset from it,
+// below 2^31.
+template <int POL>
+__device__ __forceinline__ void store16_policy(void *base, uint32_t off, const uint4 &u)
 {
     typedef unsigned int v4u __attribute__((ext_vector_type(4)));
-    constexpr int kSc0Sc1 = 1 | 16;            // cache-policy bits: sc0, sc1
     constexpr int kRawDword3 = 0x00020000;     // raw buffer: 32-bit data format, no swizzle
     const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(base, (short)0, 0x7FFFFFFF, kRawDword3);
     const v4u v = {u.x, u.y, u.z, u.w};
-    __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)off, 0, kSc0Sc1);
+    __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)off, 0, POL);
+}
+
+// Store of a generated or injected output: non-temporal at device scope
+// (nt sc1). It streams as fast as an allocating store and leaves no dirty
+// lines of the output in the Infinity Cache. A kernel that reads an output
+// still dirty there pays for it: on gfx950 a 1 GiB check right after the
+// generation that wrote its operands with allocating stores took 222 us
+// against 172 us once they had left the cache, and 173 us after this store.
+__device__ __forceinline__ void store16_stream(void *base, uint32_t off, const uint4 &u)
+{
+    constexpr int kNtSc1 = 2 | 16;
+    store16_policy<kNtSc1>(base, off, u);
+}
+
+// Store of the cache flush: system scope (sc0 sc1), written through L2
+// without allocating there and allocated in the Infinity Cache like an
+// ordinary store (~2% faster than one for streamed writes), so the flush
+// evicts that cache's previous contents.
+__device__ __forceinline__ void store16_alloc(void *base, uint32_t off, const uint4 &u)
+{
+    constexpr int kSc0Sc1 = 1 | 16;
+    store16_policy<kSc0Sc1>(base, off, u);
 }
 
 // ---------------------------------------------------------------- narrowing
