@@ -2,7 +2,8 @@
 table (copy-calibrated FETCH_SIZE / WRITE_SIZE, and exact read bytes from the
 read-request counters by size) and the vector-issue model of the generation
 kernels (per-unit instruction path of the gfx950 assembly, weighted by issue
-cost, against the launch's waves and duration)."""
+cost, against the launch's waves and duration); and, in the same assembly,
+the cache policy of every streaming 16-byte store."""
 import csv
 import json
 import os
@@ -88,12 +89,39 @@ def test_issue_costs_cover_the_hot_instructions():
     assert P._op_cost("v_unmeasured_op", rates) == 4.0
 
 
-def test_issue_model_of_a_generation_launch(tmp_path):
+@pytest.fixture(scope="module")
+def asm():
+    """gfx950 assembly of kernels.hip, built with the library's flags."""
+    from paper_2609_30057_amd import build as B
+    return open(B.emit_asm(os.path.join(B.BUILD, "kernels_test.s"))).read()
+
+
+def _kernel_body(asm, prefix):
+    """(symbol, body) of every kernel whose mangled name starts with prefix."""
+    import re
+    return re.findall(r"^(" + re.escape(prefix) + r"\w*):(.*?)\.Lfunc_end", asm, re.S | re.M)
+
+
+def test_store_cache_policies(asm):
+    """Generated and injected outputs leave the Infinity Cache clean
+    (non-temporal device-scope stores, nt sc1); only the flush allocates
+    there (sc0 sc1), since evicting that cache is its job."""
+    import re
+    kinds = {"_ZN4krex5k_genI": "nt sc1", "_ZN4krex12k_gen_packedI": "nt sc1", "_ZN4krex8k_injectI": "nt sc1",
+             "_ZN4krex12k_gen_injectI": "nt sc1", "_ZN4krex7k_flushE": "sc0 sc1"}
+    for prefix, policy in kinds.items():
+        bodies = _kernel_body(asm, prefix)
+        assert bodies, prefix
+        for sym, body in bodies:
+            stores = re.findall(r"buffer_store_dwordx4[^\n]*", body)
+            assert stores, sym
+            assert all(st.rstrip().endswith(" " + policy) for st in stores), (sym, stores[:2])
+
+
+def test_issue_model_of_a_generation_launch(tmp_path, asm):
     """The unit path of the fp32 uniform kernel (power-of-two range) holds
     Philox's 32x32->64 multiplies and three-way xors, and the model's time is
     waves x weighted cycles over 1024 SIMDs x 2.4 GHz."""
-    from paper_2609_30057_amd import build as B
-    asm = open(B.emit_asm(os.path.join(B.BUILD, "kernels_test.s"))).read()
     ops = P._unit_path(asm, "_ZN4krex5k_genILi0ELi0ELb1EEEvNS_9GenParamsE")
     assert ops.count("v_mad_u64_u32") >= 18 and ops.count("v_bitop3_b32") >= 18
     assert any(o.startswith("v_fma") for o in ops)              # the fused uniform transform
