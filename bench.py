@@ -14,7 +14,7 @@ Metric: generate + check + flush GB/s = algorithmic bytes of those kernels
 their summed device time, measured with HIP events on the stream they run
 on. The roofline object is for the dominant kernel (the flush: 200 GiB of
 the step's 200.2 GiB). The timed-region inflation half of the metric is
-measured by `--fidelity` (Section 6.3, Eq. 1), which prints its own line.
+measured by `--fidelity` (Section 6.4, Eq. 1), which prints its own line.
 
 The default run also measures that half briefly after the timed steps
 (`inflation_p95_1ms`: 1 ms probes, 1000 single-shot samples in regions, a

@@ -112,8 +112,12 @@ typedef struct krex_check_result {
 #define KREX_ATTACH_CPU_EXCLUSIVE 2u
 krex_status krex_attach(int32_t device, const char *shm_name, uint32_t flags);
 
-/* Waits for this process's in-flight work, releases its slot and the
- * mapping. Returns KREX_ESTATE inside a region or when not attached. */
+/* Ends the registration krex_attach made (Section 4.2: each process
+ * registers with the GPU's coordinator, serialised with gate closure; this
+ * is the inverse step, so later drains stop looking at it). Waits for this process's
+ * in-flight work so no count is left behind, then releases its slot and the
+ * mapping. Returns KREX_ESTATE inside a region or when not attached,
+ * KREX_ETIMEDOUT if its work has not finished within 60 s. */
 krex_status krex_detach(void);
 
 /* --- generation -----------------------------------------------------------
@@ -233,7 +237,7 @@ krex_status krex_flush(void *buf, uint64_t bytes, uint32_t pattern, void *stream
  * A known-work timed kernel: 256 blocks x 256 threads, each thread runs 8
  * independent fp32 FMA chains for `iters` steps and writes their sum to
  * sink[thread] (device, 65536 floats). Used to measure timing inflation
- * (Section 6.3, Eq. 1). */
+ * (Section 6.4, Eq. 1). */
 #define KREX_PROBE_THREADS 65536
 krex_status krex_probe(uint64_t iters, float *sink, void *stream);
 

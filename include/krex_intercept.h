@@ -3,11 +3,11 @@
  * library that gates every kernel dispatch of a process (torch kernels,
  * library GEMMs, HIP's copy kernels), not only this library's own launches.
  *
- * Paper, Section 5 (AMD): queue creation is replaced through the runtime's
- * dispatch table so that each queue's kernel launches pass through the
- * interposer; an in-flight counter is incremented on submission and
- * decremented by a polling thread when the operation's completion signal
- * fires; tenants join after their initialisation.
+ * Paper, Section 5 (AMD): the interposer swaps queue creation in the
+ * runtime's dispatch table, so every kernel launch of every queue passes
+ * through it; a launch batch raises the process's in-flight count and a
+ * poller thread lowers it when the batch's completion signal reports the
+ * work done; a tenant joins only after its initialisation.
  *
  * Use: start the tenant with HSA_TOOLS_LIB=<path>/libkrex_intercept.so and
  * KREX_INTERCEPT_SHM=<segment name> (the coordinator segment of

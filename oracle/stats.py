@@ -1,6 +1,6 @@
 """Timing statistics of the paper's fidelity metric -- TEST INFRASTRUCTURE.
 
-Eq. 1 (Section 6.3): P = p95(r) - 1 with r = t_measured / t_native, reported
+Eq. 1 (Section 6.4): P = p95(r) - 1 with r = t_measured / t_native, reported
 as a percentage. The paper does not name a percentile method; the reading
 here is linear interpolation between order statistics (position
 q (n - 1) in the sorted sample), written out plainly. Section 2.1 names the

@@ -2,11 +2,10 @@
 // gate around every launch, device-completion tracking of counted work,
 // region entry and exit, and the timed loop.
 //
-// Completion tracking follows the AMD variant of the paper (Section 5): the
-// in-flight counter is incremented when an operation is admitted and
-// decremented by a polling thread when the operation's completion signal
-// fires; here the signal is a HIP event recorded after the launch and the
-// thread blocks on it. A failed launch releases its count at once (Section
+// Completion tracking follows the AMD variant of the paper (Section 5): a
+// launch raises the process's in-flight count when it is admitted, and the
+// count drops when the HIP event recorded right after the launch completes,
+// observed by one tracking thread per process that blocks on such events. A failed launch releases its count at once (Section
 // 4.2: decrement on error returns too).
 #include <hip/hip_runtime.h>
 #include <math.h>

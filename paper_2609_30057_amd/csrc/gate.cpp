@@ -669,9 +669,9 @@ int region_begin(uint32_t timeout_ms)
     s.region_gate = seg->gate.load(std::memory_order_seq_cst);
     s.last_frozen.store(0);
     if (s.flags & kCpuExclusive) {
-        // Step 4: stop the siblings' process trees once their GPU work has
-        // drained, recording in each slot the region that stopped it so that
-        // cleanup after this holder's death resumes exactly these.
+        // Step 4: with every sibling's in-flight count at zero, stop their
+        // process trees; each stopped slot records this region's gate word,
+        // so a recovery after this holder's death resumes exactly these.
         const int32_t self = (int32_t)getpid();
         const uint64_t until = now_ns() + 20000000ull;
         uint64_t frozen = 0;

@@ -3,13 +3,13 @@
 // the process calls this library's C ABI (torch kernels, library GEMMs, HIP's
 // own copy kernels).
 //
-// Paper, Section 5 (AMD): a ROCm tools library replaces queue creation in
-// the runtime's dispatch table so that every queue's kernel launches pass
-// through the interposer; the in-flight counter is incremented when an
-// operation is submitted and decremented by a polling thread when the
-// operation's completion signal fires; the holder waits for the counters to
-// reach zero (Section 4.2, step 3). Tenants register after initialisation
-// (here: at their first dispatch).
+// Paper, Section 5 (AMD): the interposer is a ROCm tools library that swaps
+// queue creation in the runtime's dispatch table, so every kernel launch of
+// every queue is seen on its way to the GPU. Each launch batch raises the
+// process's in-flight count; a poller thread lowers it once the batch's
+// completion signal reports the work done, and a region holder waits for
+// every other process's count to reach zero (Section 4.2, step 3). A tenant
+// joins only after its initialisation (here: at its first dispatch).
 //
 // Mechanism: loaded by the HSA runtime through HSA_TOOLS_LIB, OnLoad swaps
 // hsa_queue_create for a wrapper that creates an intercept queue and

@@ -14,7 +14,7 @@
 //   k_flush   16-byte allocating stores of a pattern (Section 2.1 flush
 //             between iterations; Section 4.2 step 5).
 //   k_probe   fixed-work FMA kernel timed by the fidelity measurement
-//             (Section 6.3, Eq. 1).
+//             (Section 6.4, Eq. 1).
 //   k_sgemm   naive fp32 GEMM standing in for a candidate kernel.
 //
 // Work is laid out block-contiguously in address order (block b owns units

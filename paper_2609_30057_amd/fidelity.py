@@ -1,9 +1,9 @@
 """Shared-GPU timing fidelity: p95 inflation of probe kernels timed inside
 critical regions while sibling processes generate and check on the same GPU.
 
-Paper: Section 6.3 (Eq. 1, P = p95(t_measured / t_native) - 1, with a second
-native run as the control for run-to-run noise); Section 6.4 (fidelity by
-kernel duration, 0.1 / 1 / 10 ms); Section 6.5 (ungated sharing as the
+Paper: Section 6.4 (Eq. 1, P = p95(t_measured / t_native) - 1, with a second
+native run as the control for run-to-run noise, and fidelity by kernel
+duration, 0.1 / 1 / 10 ms); Section 6.5 (ungated sharing as the
 unprotected baseline); Section 6.6 (single-shot and median-of-ten timing).
 
 Procedure, on one GPU:

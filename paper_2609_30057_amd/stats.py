@@ -1,6 +1,6 @@
 """Timing statistics of the fidelity measurement.
 
-Section 6.3, Eq. 1: P = p95(r) - 1, r = t_measured / t_native, with the p95
+Section 6.4, Eq. 1: P = p95(r) - 1, r = t_measured / t_native, with the p95
 taken by linear interpolation between order statistics (numpy's default).
 Section 6.6: single-shot timing and median-of-ten timing.
 """

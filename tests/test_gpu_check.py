@@ -142,11 +142,67 @@ def test_max_rel_search_matches_oracle(kind):
     an infinite ratio in the n mod E tail or just before it."""
     for n in (1003, (1 << 20) + 5):
         a, b = _ratio_inputs(kind, n, 5)
-        for dta, dtb in (("f32", "f32"), ("f16", "f32"), ("bf16", "bf16"), ("f8", "f16")):
+        for dta, dtb in (("f32", "f32"), ("f16", "f32"), ("bf16", "bf16"), ("f8", "f16"), ("f8", "f8")):
             ac = oracle.from_f32(a, dta) if dta != "f32" else a
             bc = oracle.from_f32(b, dtb) if dtb != "f32" else b
             ref = oracle.check(ac, dta, bc, dtb, 1e-3, 1e-5)
             r = krex.check(from_storage(ac, dta), from_storage(bc, dtb), 1e-3, 1e-5)
+            same_result(r, ref)
+
+
+def _f8_pairs(kind, n, seed):
+    """fp8 e4m3fn operand pairs for the fp8 x fp8 max_rel filter: every
+    ordered pair of finite fp8 codes (b the reference), arranged so the
+    filter's bound is tested at its edge -- ratios rising along the index
+    (every chunk raises the maximum), falling (the maximum comes first),
+    only the pairs of the largest finite ratio below +inf spread over the
+    whole array (ties within and across waves), a random arrangement, and
+    subnormal references only. Ratios are ordered exactly (fp64 of fp8
+    values is exact)."""
+    codes = np.array([c for c in range(256) if c not in (0x7F, 0xFF)], dtype=np.uint8)
+    av = oracle.to_f32(codes, "f8").astype(np.float64)
+    A, B = np.meshgrid(codes, codes, indexing="ij")
+    Av, Bv = np.meshgrid(av, av, indexing="ij")
+    A, B, Av, Bv = A.ravel(), B.ravel(), Av.ravel(), Bv.ravel()
+    d = np.abs(Av - Bv)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        ratio = np.where(d == 0, 0.0, np.where(Bv == 0, np.inf, d / np.abs(Bv)))
+    rng = np.random.default_rng(seed)
+    if kind == "subnormal":
+        keep = (B & 0x78) == 0          # exponent field 0: zero or subnormal references
+        A, B, ratio = A[keep], B[keep], ratio[keep]
+    if kind in ("rising", "falling", "ties"):
+        fin = np.isfinite(ratio)
+        A, B, ratio = A[fin], B[fin], ratio[fin]
+    if kind == "ties":
+        top = ratio.max()
+        sel = np.nonzero(ratio == top)[0]
+        low = np.nonzero(ratio < top)[0]
+        idx = rng.choice(low, n)
+        idx[rng.random(n) < 0.01] = rng.choice(sel, 1)[0]
+        return A[idx], B[idx]
+    if kind == "random":
+        idx = rng.integers(0, A.size, n)
+        return A[idx], B[idx]
+    order = np.argsort(ratio, kind="stable")
+    if kind == "falling":
+        order = order[::-1]
+    if kind == "subnormal":
+        order = rng.permutation(A.size)
+    pos = (np.arange(n, dtype=np.int64) * order.size) // n
+    return A[order[pos]], B[order[pos]]
+
+
+@pytest.mark.parametrize("kind", ["rising", "falling", "ties", "random", "subnormal"])
+def test_max_rel_search_fp8_pairs(kind):
+    """fp8 x fp8 is the one pair whose max_rel candidate filter is a single
+    product with a rounded-up 1/R (no infinity, no overflow): max_rel and
+    every other field at 0 ULP on arrangements of every finite fp8 pair."""
+    for n in (1003, (1 << 20) + 5):
+        a, b = _f8_pairs(kind, n, 9)
+        for rtol, atol in ((1e-3, 1e-5), (0.125, 0.125)):
+            ref = oracle.check(a, "f8", b, "f8", rtol, atol)
+            r = krex.check(from_storage(a, "f8"), from_storage(b, "f8"), rtol, atol)
             same_result(r, ref)
 
 

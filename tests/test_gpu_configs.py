@@ -121,4 +121,9 @@ def test_mixed_stream_commands():
                 assert_bits_equal(to_storage(x[start:start + m], dt), xr, what + " x window")
                 yr, _ = oracle.inject(xr, dt, c.mask_seed, c.rate, cfg["delta"], oracle.INJ_ROUND, start)
                 assert_bits_equal(to_storage(y[start:start + m], dt), yr, what + " y window")
+            # the record itself, on the GPU's own tensors copied back: the
+            # oracle's check of exactly the bytes the GPU check read
+            xs, ys = to_storage(x, dt), to_storage(y, dt)
+            same_result(r, oracle.check(ys, dt, xs, dt, c.rtol, c.atol))
+            del xs, ys
             assert r.n == c.n and r.nan_count == 0

@@ -1,4 +1,4 @@
-"""Pins the oracle's timing statistics (Eq. 1 of Section 6.3) on hand-worked
+"""Pins the oracle's timing statistics (Eq. 1 of Section 6.4) on hand-worked
 samples, and against numpy's default (linear) percentile."""
 import numpy as np
 

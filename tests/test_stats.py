@@ -1,4 +1,4 @@
-"""The benchmark's timing statistics (Eq. 1 of Section 6.3) against the
+"""The benchmark's timing statistics (Eq. 1 of Section 6.4) against the
 oracle's plainly written version, on random samples and hand-worked ones."""
 import numpy as np
 
