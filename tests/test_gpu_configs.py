@@ -108,6 +108,7 @@ def test_mixed_stream_commands():
         krex.inject(y, x, c.mask_seed, c.rate, cfg["delta"], "round")
         r = krex.check(y, x, c.rtol, c.atol)
         what = "command %d (%s n=%d)" % (c.index, dt, c.n)
+        print(what, flush=True)
         if c.n <= (1 << 25):
             xr = oracle.gen(dt, c.n, c.value_seed, 0, c.dist, c.p0, c.p1)
             assert_bits_equal(to_storage(x, dt), xr, what + " x")
