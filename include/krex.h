@@ -198,6 +198,23 @@ krex_status krex_gen_inject(void *x, void *y, int32_t dtype, uint64_t n, uint64_
 krex_status krex_check(const void *a, int32_t dta, const void *b, int32_t dtb, uint64_t n, float rtol,
                        float atol, krex_check_result *out, void *stream);
 
+/* krex_check without allocation, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same arguments, checks and result, field for
+ * field, but the block partials the check reduces live in a fixed device
+ * array of the library (4096 partials, 128 KiB per GPU, held until the
+ * process ends) instead of a per-stream buffer allocated on first use. It
+ * calls no hipMalloc / hipFree. Every size krex_check accepts fits in the
+ * array (n < 2^33; larger n returns KREX_EINVAL), and no partial needs
+ * clearing: each call writes the ones it reads. All calls on one GPU share
+ * the array, so two calls that may overlap on one GPU (on different
+ * streams, or from different threads without ordering) race and can return
+ * wrong records; calls ordered on one stream are safe. When the process is
+ * attached with gating, completion is tracked with a HIP event from the
+ * library's event pool, as for every entry point. */
+krex_status krex_check_noalloc(const void *a, int32_t dta, const void *b, int32_t dtb, uint64_t n, float rtol,
+                               float atol, krex_check_result *out, void *stream);
+
 /* The same check against a reference that is regenerated instead of read:
  * *out equals krex_check(a, dta, b, dtb, n, rtol, atol) for the b that
  * krex_gen(b, dtb, n, seed, offset, dist, p0, p1) writes, field for field,

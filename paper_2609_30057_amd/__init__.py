@@ -112,6 +112,7 @@ def lib():
             "krex_inject": (i32, [vp, vp, i32, u64, u64, u64, f64, f32, i32, vp]),
             "krex_gen_inject": (i32, [vp, vp, i32, u64, u64, u64, i32, f32, f32, u64, u64, f64, f32, i32, vp]),
             "krex_check": (i32, [vp, i32, vp, i32, u64, f32, f32, vp, vp]),
+            "krex_check_noalloc": (i32, [vp, i32, vp, i32, u64, f32, f32, vp, vp]),
             "krex_check_gen": (i32, [vp, i32, i32, u64, u64, u64, i32, f32, f32, f32, f32, vp, vp]),
             "krex_check_gen_packed": (i32, [vp, i32, i32, u64, u64, u64, i32, f32, f32, f32, f32, vp, vp]),
             "krex_flush": (i32, [vp, u64, u32, vp]),
@@ -274,6 +275,20 @@ def check(a, b, rtol, atol, out=None, stream=None, sync=True):
         out = check_result_buffer(a.device)
     _chk(lib().krex_check(_dev(a), dtype_code(a.dtype), _dev(b), dtype_code(b.dtype), a.numel(), float(rtol),
                           float(atol), _dev(out), _stream(stream)), "krex_check")
+    if not sync:
+        return out
+    return decode_check_result(out)
+
+
+def check_noalloc(a, b, rtol, atol, out, stream=None, sync=True):
+    """check() through krex_check_noalloc: the library allocates nothing (its
+    partials live in a fixed device array shared by every call on the GPU;
+    overlapping calls on one GPU race). `out` is the caller's result buffer
+    (check_result_buffer()). With sync=False returns `out` undecoded."""
+    if a.numel() != b.numel():
+        raise ValueError("a and b must have the same number of elements")
+    _chk(lib().krex_check_noalloc(_dev(a), dtype_code(a.dtype), _dev(b), dtype_code(b.dtype), a.numel(),
+                                  float(rtol), float(atol), _dev(out), _stream(stream)), "krex_check_noalloc")
     if not sync:
         return out
     return decode_check_result(out)

@@ -430,6 +430,25 @@ krex_status krex_check(const void *a, int32_t dta, const void *b, int32_t dtb, u
     return submit(s, [&] { return krex::launch_check(a, dta, b, dtb, n, rtol, atol, scratch, out, s); });
 }
 
+krex_status krex_check_noalloc(const void *a, int32_t dta, const void *b, int32_t dtb, uint64_t n, float rtol,
+                               float atol, krex_check_result *out, void *stream)
+{
+    const size_t sa = elem_size(dta), sb = elem_size(dtb);
+    if (sa == 0 || sb == 0 || dta == KREX_U32 || dtb == KREX_U32) return KREX_EINVAL;
+    if (!(rtol >= 0.0f) || !(atol >= 0.0f) || !finite_f(rtol) || !finite_f(atol)) return KREX_EINVAL;
+    // the fixed scratch holds the partials of every grid the check uses, so
+    // the size limit is the check's own: n < 2^33
+    if (n >= (1ull << 33)) return KREX_EINVAL;
+    if (!out) return KREX_EINVAL;
+    if (n > 0 && (!a || !b)) return KREX_EINVAL;
+    if (!aligned(a, sa) || !aligned(b, sb) || !aligned(out, 8)) return KREX_EALIGN;
+    hipStream_t s = (hipStream_t)stream;
+    void *scratch = nullptr;
+    const hipError_t e = krex::noalloc_scratch(&scratch);
+    if (e != hipSuccess) return hip_fail(e);
+    return submit(s, [&] { return krex::launch_check(a, dta, b, dtb, n, rtol, atol, scratch, out, s); });
+}
+
 krex_status krex_check_gen(const void *a, int32_t dta, int32_t dtb, uint64_t n, uint64_t seed, uint64_t offset,
                            int32_t dist, float p0, float p1, float rtol, float atol, krex_check_result *out,
                            void *stream)

@@ -28,6 +28,7 @@
 #include <stdlib.h>
 
 #include <cmath>
+#include <mutex>
 
 #include "check_device.hpp"
 #include "hip_launch.hpp"
@@ -800,6 +801,37 @@ hipError_t launch_gen_inject(void *x, void *y, int dt, uint64_t n, uint64_t seed
 // check_device.hpp; k_check takes the reference from memory.
 
 size_t check_scratch_bytes() { return (size_t)kMaxCheckBlocks * sizeof(CheckPartial); }
+
+// The fixed partial buffer of krex_check_noalloc: one CheckPartial per check
+// block, kMaxCheckBlocks of them (128 KiB), the most any check grid uses.
+// Each GPU the library runs on holds its own copy until the process ends.
+// Host code never passes this name to a kernel (on the host it is only a
+// stand-in for the symbol); it passes the device address that
+// noalloc_scratch() looks up once per device.
+static __device__ __align__(256) CheckPartial scratch[kMaxCheckBlocks];
+
+static_assert(sizeof(scratch) == (size_t)kMaxCheckBlocks * sizeof(CheckPartial), "noalloc scratch size");
+
+hipError_t noalloc_scratch(void **out)
+{
+    static std::mutex mu;
+    static void *addr[kMaxDevices] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> g(mu);
+    if (!addr[dev]) {
+        // with `dev` current: its own copy of the array
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        addr[dev] = p;
+    }
+    *out = addr[dev];
+    return hipSuccess;
+}
 
 // Reference operand in memory.
 template <int DA, int DB, bool VEC, int D>

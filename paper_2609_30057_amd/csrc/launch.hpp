@@ -41,6 +41,13 @@ hipError_t launch_gen_inject(void *x, void *y, int dt, uint64_t n, uint64_t seed
 // The check reduces per-block partials held in `scratch` (device memory of
 // check_scratch_bytes()); calls that may overlap need distinct scratch.
 size_t check_scratch_bytes();
+// Devices the library keeps per-device state for.
+static constexpr int kMaxDevices = 64;
+// The device address, on the current device, of the library's fixed check
+// scratch (check_scratch_bytes() bytes, a file-scope device array), looked
+// up once per device and cached. Used by krex_check_noalloc in place of an
+// allocated buffer; every call on one device shares it.
+hipError_t noalloc_scratch(void **out);
 hipError_t launch_check(const void *a, int dta, const void *b, int dtb, uint64_t n, float rtol, float atol,
                         void *scratch, krex_check_result *out, hipStream_t s);
 // The check of a against the reference krex_gen would write for (dtb,
