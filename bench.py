@@ -16,15 +16,21 @@ on. The roofline object is for the dominant kernel (the flush: 200 GiB of
 the step's 200.2 GiB). The timed-region inflation half of the metric is
 measured by `--fidelity` (Section 6.4, Eq. 1), which prints its own line.
 
-The default run also measures that half briefly after the timed steps
+The default line also carries the commands whose bytes are generation and
+check rather than flush, at full size: `check_stress` (2 GiB: generation,
+injection and check of 268M fp16 elements, separately and with generation
+and injection fused, each kernel's fraction of 8 TB/s) and `mixed_stream`
+(64 commands, about 73 GB). It then measures the timing half briefly
 (`inflation_p95_1ms`: 1 ms probes, 1000 single-shot samples in regions, a
 native repeat and 7 gated sibling processes), unless --no-fidelity.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--no-fidelity]
-       python bench.py --fidelity [--samples S] [--siblings N] [--warmup-ms W]
+       python bench.py --fidelity [--samples S] [--siblings N] [--warmup-ms W] [--warmup-mode time|clock]
+                              [--sessions K] [--durations 0.1,1,10]
                               [--modes control,gated,ungated,frozen,frozen_nopin,torch_gated,torch_ungated]
        python bench.py --kernels          per-kernel throughput on the command shapes
        python bench.py --configs          the other commands: gemm_tiny, check_stress, mixed_stream
+       python bench.py --cache-probe      reads warm / after a flush / cold: what the flush evicts
        python bench.py --calib-copy       also time a plain 1 GiB device copy (the
                                           reference kernel for rocprofv3 byte counters)
        python bench.py --valu-rates       issue cost of the vector instructions the kernels
@@ -62,10 +68,51 @@ def _traffic_for(kernel_key):
     return ent.get("hbm_bytes_per_launch")
 
 
+def host_facts():
+    """The host the oracle runs on: logical CPUs, the CPUs this process may
+    use, and the CPU model."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"host_cpus": os.cpu_count(), "allowed_cpus": len(os.sched_getaffinity(0)), "cpu_model": model}
+
+
+class pinned_core:
+    """Runs the block on one core of this process's affinity set (the
+    highest-numbered one): the calling thread's affinity is set in-process
+    and restored afterwards, so the single-threaded oracle stays on one
+    core."""
+
+    def __enter__(self):
+        self.saved = os.sched_getaffinity(0)
+        self.core = max(self.saved)
+        os.sched_setaffinity(0, {self.core})
+        return self
+
+    def __exit__(self, *exc):
+        os.sched_setaffinity(0, self.saved)
+        return False
+
+
 def cpu_baseline(step_bytes):
     """The oracle (single-threaded C) on a bounded sample of one step: both
     generated matrices and the full check, plus 20 of the 200 1 GiB flushes
-    (host fill of a pre-touched buffer), scaled to one step's byte mix."""
+    (host fill of a pre-touched buffer), scaled to one step's byte mix. Runs
+    pinned to one core."""
+    with pinned_core() as pc:
+        out = _cpu_baseline(step_bytes)
+    out.update(host_facts())
+    out["core"] = pc.core
+    return out
+
+
+def _cpu_baseline(step_bytes):
     import numpy as np
     import oracle
     from paper_2609_30057_amd import workloads as W
@@ -95,8 +142,9 @@ def cpu_baseline(step_bytes):
         "cores": 1,
         "kind": "oracle",
         "sample": ("one gemm_large step on the host: generation of both 4096x4096 bf16 normal matrices "
-                   "(%.2f s), the full 16.8M-element bf16-vs-fp32 check (%.2f s), and 20 of the 200 1 GiB "
-                   "flush fills scaled x10 (%.2f s); single-threaded C oracle" % (t_gen, t_check, t_flush)),
+                   "(%.2f s), the full 16.8M-element bf16-vs-fp32 check against a seeded fp32 operand of "
+                   "the reference's shape (%.2f s), and 20 of the 200 1 GiB flush fills scaled x10 (%.2f s); "
+                   "single-threaded C oracle pinned to one core" % (t_gen, t_check, t_flush)),
     }
 
 
@@ -194,6 +242,8 @@ def run_gemm_large(steps, warmup, with_cpu):
                          "bf16 candidate C vs fp32 reference C checked at rtol 1.6e-2 atol 1e-2; "
                          "10 warm-up + 200 timed reps of the candidate in a critical region, 1 GiB flush "
                          "before each rep"),
+            "tensor_dtypes": "A, B, C bf16; reference C f32 (dtype names the arithmetic: fp32 transforms and "
+                             "check, u32 Philox)",
             "elements_per_matrix": n2,
             "flush_bytes": cfg["flush_bytes"],
             "reps": cfg["reps"],
@@ -246,7 +296,7 @@ def short_fidelity(samples=1000):
             "median_of_10_native_repeat": r["P_median_of_10"]["1.0"]["control"],
             "probe_ms": 1.0, "samples": samples, "siblings": r["siblings"],
             "sibling_GBps": r["sibling_GBps"].get("gated"), "drain_ms_p95": r["drain_ms"]["gated"]["p95"],
-            "target": "<= 1%"}
+            "warmup": r["warmup"], "clock": r["clock"]["1.0"], "target": "<= 1%"}
 
 
 def run_kernels():
@@ -384,18 +434,145 @@ def configs_cpu_baseline(cmds):
     return out
 
 
+def _event():
+    import torch
+    e = torch.cuda.Event(enable_timing=True)
+    e.record()
+    return e
+
+
+def _rate(nbytes, ms):
+    gbps = nbytes / (ms / 1e3) / 1e9
+    return {"ms": round(ms, 4), "GBps": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 3)}
+
+
+def measure_check_stress(reps=5):
+    """The check_stress command at full size (x fp16 16384 x 16384 uniform
+    [-4, 4), seed 2; y = EXACT inject(x, mask seed 3, rate 0.001, delta 0.5);
+    check(y, x) at rtol = atol = 1e-3), `reps` times each way: generation,
+    injection and check as three launches, and generation with injection
+    fused (x and y written in one pass) followed by the check. HIP events on
+    the launching stream around each launch, about 0.1 ms of the probe
+    kernel ahead of the first event so no event times the host's enqueue;
+    medians over the reps. Algorithmic bytes (the method's): generation and
+    injection each write 2n, the check reads 4n, 8n = 2 GiB per command
+    either way; each kernel's fraction of 8 TB/s counts the bytes it moves
+    (injection: x read and y written, 4n)."""
+    import numpy as np
+    import torch
+
+    import paper_2609_30057_amd as krex
+    from paper_2609_30057_amd import workloads as W
+
+    cfg = W.CHECK_STRESS
+    m = cfg["rows"] * cfg["cols"]
+    dev = torch.device("cuda:0")
+    x = torch.empty(m, dtype=torch.float16, device=dev)
+    y = torch.empty_like(x)
+    res = krex.check_result_buffer(dev)
+    lead = torch.empty(krex.PROBE_THREADS, dtype=torch.float32, device=dev)
+    sep, fus, verdicts = [], [], []
+    for _ in range(reps):
+        krex.probe(LEAD_PROBE_ITERS, lead)
+        e0 = _event()
+        krex.gen(x, cfg["seed"], 0, "uniform", cfg["p0"], cfg["p1"])
+        e1 = _event()
+        krex.inject(y, x, cfg["mask_seed"], cfg["rate"], cfg["delta"], "exact")
+        e2 = _event()
+        krex.check(y, x, cfg["rtol"], cfg["atol"], out=res, sync=False)
+        e3 = _event()
+        v = krex.decode_check_result(res)
+        sep.append((e0.elapsed_time(e1), e1.elapsed_time(e2), e2.elapsed_time(e3)))
+        krex.probe(LEAD_PROBE_ITERS, lead)
+        f0 = _event()
+        krex.gen_inject(x, y, cfg["seed"], 0, "uniform", cfg["p0"], cfg["p1"], mask_seed=cfg["mask_seed"],
+                        rate=cfg["rate"], delta=cfg["delta"], mode="exact")
+        f1 = _event()
+        krex.check(y, x, cfg["rtol"], cfg["atol"], out=res, sync=False)
+        f2 = _event()
+        vf = krex.decode_check_result(res)
+        fus.append((f0.elapsed_time(f1), f1.elapsed_time(f2)))
+        verdicts.append((v, vf))
+    tg, ti, tc = (float(np.median([r[k] for r in sep])) for k in range(3))
+    tf, tcf = (float(np.median([r[k] for r in fus])) for k in range(2))
+    v, vf = verdicts[-1]
+    same = all((a.mismatches, a.nan_count, a.argmax_abs, a.max_abs, a.max_rel)
+               == (b.mismatches, b.nan_count, b.argmax_abs, b.max_abs, b.max_rel)
+               == (v.mismatches, v.nan_count, v.argmax_abs, v.max_abs, v.max_rel) for a, b in verdicts)
+    alg = 8 * m
+    out = {
+        "workload": ("check_stress: x fp16 16384x16384 uniform[-4,4) seed 2; y = EXACT inject(x, mask seed 3, "
+                     "rate 0.001, delta 0.5); check(y, x) rtol 1e-3 atol 1e-3"),
+        "algorithmic_bytes": alg,
+        "reps": reps,
+        "separate": dict(_rate(alg, tg + ti + tc), kernels={
+            "gen_f16_uniform": _rate(2 * m, tg), "inject_f16_exact": _rate(4 * m, ti),
+            "check_f16_f16": _rate(4 * m, tc)}),
+        "fused": dict(_rate(alg, tf + tcf), kernels={
+            "gen_inject_f16": _rate(4 * m, tf), "check_f16_f16": _rate(4 * m, tcf)}),
+        "verdict": {"mismatches": v.mismatches, "nan_count": v.nan_count, "argmax_abs": v.argmax_abs,
+                    "max_abs": v.max_abs, "max_rel": v.max_rel},
+        "verdict_same_every_rep_and_path": bool(same),
+    }
+    del x, y
+    return out
+
+
+def measure_mixed_stream():
+    """The mixed_stream command: 64 commands derived from the words of seed 4
+    (1 MiB - 1 GiB, the four dtypes, uniform or normal, 0-1% ROUND
+    injection with delta 1.0); each runs generation with injection in one
+    call, the check with its verdict read back, and a 512 MiB flush. GB/s of
+    the algorithmic bytes (4 bytes per byte of tensor: x and y written, both
+    read by the check; plus the flush) over the summed event time of the
+    command's launches, and over the wall clock (launches and verdict
+    readback included)."""
+    import numpy as np
+    import torch
+
+    import paper_2609_30057_amd as krex
+    from paper_2609_30057_amd import workloads as W
+
+    cfg = W.MIXED_STREAM
+    dev = torch.device("cuda:0")
+    res = krex.check_result_buffer(dev)
+    fl512 = torch.empty(cfg["flush_bytes"] // 4, dtype=torch.int32, device=dev)
+    w = torch.empty(1024, dtype=torch.int32, device=dev)
+    krex.gen(w, cfg["seed"], 0)
+    cmds = W.mixed_stream_commands(w.cpu().numpy().view(np.uint32))
+    xbuf = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    ybuf = torch.empty_like(xbuf)
+    tdt = {0: torch.float32, 1: torch.bfloat16, 2: torch.float16, 3: torch.float8_e4m3fn}
+    torch.cuda.synchronize()
+    kernel_ms, total, mism = 0.0, 0, 0
+    t0 = time.perf_counter()
+    for c in cmds:
+        xv = xbuf[:c.nbytes].view(tdt[c.dtype])
+        yv = ybuf[:c.nbytes].view(tdt[c.dtype])
+        e0 = _event()
+        krex.gen_inject(xv, yv, c.value_seed, 0, c.dist, c.p0, c.p1, mask_seed=c.mask_seed, rate=c.rate,
+                        delta=cfg["delta"], mode="round")
+        krex.check(yv, xv, c.rtol, c.atol, out=res, sync=False)
+        krex.flush(fl512)
+        e1 = _event()
+        mism += krex.decode_check_result(res).mismatches
+        kernel_ms += e0.elapsed_time(e1)
+        total += c.nbytes * 4 + cfg["flush_bytes"]
+    wall = time.perf_counter() - t0
+    del xbuf, ybuf
+    return cmds, {"workload": "mixed_stream: 64 commands from the words of seed 4, 1 MiB-1 GiB, fp32/bf16/fp16/fp8, "
+                              "uniform[-1,1) or normal(0,1), ROUND injection 0-1% delta 1.0, 512 MiB flush each",
+                  "algorithmic_bytes": total, "GBps": round(total / (kernel_ms / 1e3) / 1e9, 1),
+                  "frac_hbm": round(total / (kernel_ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 3),
+                  "wall_GBps": round(total / wall / 1e9, 1), "commands_per_s": round(len(cmds) / wall, 1),
+                  "mismatches_total": int(mism)}
+
+
 def run_configs(with_cpu=True):
     """The other commands end to end: gemm_tiny (gen + check + 100 reps with a
-    512 MiB flush in a region), check_stress (gen + inject + check of 256M
-    fp16), mixed_stream (64 derived commands: gen and inject in one call,
-    check with the verdict read back, 512 MiB flush). GB/s = algorithmic bytes / summed
-    event time of the hot-path kernels, the bytes as the method defines
-    them: generation and injection each write n elements (injection's read
-    of x is not counted, x could be regenerated), the check reads both
-    operands, the flush writes its buffer. The per-kernel rates beside them
-    (gen_GBps, inject_GBps, check_GBps) count the bytes each kernel moves
-    (injection: x read and y written). mixed_stream also reports wall
-    commands/s including launches and verdict readback."""
+    512 MiB flush in a region), check_stress (measure_check_stress) and
+    mixed_stream (measure_mixed_stream), with the oracle on one core beside
+    them."""
     import numpy as np
     import torch
 
@@ -409,11 +586,6 @@ def run_configs(with_cpu=True):
     out = {"metric": "per-command gen+check+flush GB/s", "unit": "GB/s", "commands": {}}
     res = krex.check_result_buffer(dev)
 
-    def ev():
-        e = torch.cuda.Event(enable_timing=True)
-        e.record()
-        return e
-
     # gemm_tiny
     cfg = W.GEMM_TINY
     n = cfg["n"]
@@ -426,12 +598,12 @@ def run_configs(with_cpu=True):
     krex.gen(B, cfg["seed"], offB)
     Cref = torch.matmul(A.cpu(), B.cpu()).to(dev)          # the command's fp32 CPU reference
     krex.fixture_sgemm(A, B, C)
-    e0 = ev()
+    e0 = _event()
     krex.gen(A, cfg["seed"], offA)
     krex.gen(B, cfg["seed"], offB)
-    e1 = ev()
+    e1 = _event()
     krex.check(C.view(-1), Cref.view(-1), cfg["rtol"], cfg["atol"], out=res, sync=False)
-    e2 = ev()
+    e2 = _event()
     times, ftimes = krex.time_loop(krex.sgemm_launcher(A, B, C), cfg["warmup"], cfg["reps"], flush_buf=fl512,
                                    region=True, with_flush_times=True)
     v = krex.decode_check_result(res)
@@ -440,82 +612,94 @@ def run_configs(with_cpu=True):
     out["commands"]["gemm_tiny"] = {"GBps": round(nbytes / t / 1e9, 1), "bytes": nbytes,
                                     "candidate_median_ms": round(float(np.median(times)), 4),
                                     "mismatches": v.mismatches, "max_abs": v.max_abs}
-    del A, B, C, Cref
-
-    # check_stress
-    cfg = W.CHECK_STRESS
-    m = cfg["rows"] * cfg["cols"]
-    x = torch.empty(m, dtype=torch.float16, device=dev)
-    y = torch.empty_like(x)
-    for _ in range(2):
-        e0 = ev()
-        krex.gen(x, cfg["seed"], 0, "uniform", cfg["p0"], cfg["p1"])
-        e1 = ev()
-        krex.inject(y, x, cfg["mask_seed"], cfg["rate"], cfg["delta"], "exact")
-        e2 = ev()
-        krex.check(y, x, cfg["rtol"], cfg["atol"], out=res, sync=False)
-        e3 = ev()
-        v = krex.decode_check_result(res)
-    tg, ti, tc = e0.elapsed_time(e1), e1.elapsed_time(e2), e2.elapsed_time(e3)
-    nbytes = m * 2 + m * 2 + m * 4
-    # the same command with generation and injection fused (x and y written
-    # in one pass, x not read back): 8 bytes per element moved instead of 10
-    for _ in range(2):
-        f0 = ev()
-        krex.gen_inject(x, y, cfg["seed"], 0, "uniform", cfg["p0"], cfg["p1"], mask_seed=cfg["mask_seed"],
-                        rate=cfg["rate"], delta=cfg["delta"], mode="exact")
-        f1 = ev()
-        krex.check(y, x, cfg["rtol"], cfg["atol"], out=res, sync=False)
-        f2 = ev()
-        vf = krex.decode_check_result(res)
-    tf, tcf = f0.elapsed_time(f1), f1.elapsed_time(f2)
-    out["commands"]["check_stress_fused"] = {
-        "GBps": round(m * 8 / ((tf + tcf) / 1e3) / 1e9, 1), "bytes": m * 8, "ms": round(tf + tcf, 4),
-        "gen_inject_GBps": round(m * 4 / (tf / 1e3) / 1e9, 1), "check_GBps": round(m * 4 / (tcf / 1e3) / 1e9, 1),
-        "mismatches": vf.mismatches, "max_abs": vf.max_abs, "argmax_abs": vf.argmax_abs,
-        "same_record_as_separate": (vf.mismatches, vf.max_abs, vf.argmax_abs, vf.nan_count)
-        == (v.mismatches, v.max_abs, v.argmax_abs, v.nan_count)}
-    out["commands"]["check_stress"] = {
-        "ms": round(tg + ti + tc, 4),
-        "GBps": round(nbytes / ((tg + ti + tc) / 1e3) / 1e9, 1), "bytes": nbytes,
-        "gen_GBps": round(m * 2 / (tg / 1e3) / 1e9, 1), "inject_GBps": round(m * 4 / (ti / 1e3) / 1e9, 1),
-        "check_GBps": round(m * 4 / (tc / 1e3) / 1e9, 1), "mismatches": v.mismatches, "max_abs": v.max_abs,
-        "argmax_abs": v.argmax_abs}
-
-    # mixed_stream
-    cfg = W.MIXED_STREAM
-    w = torch.empty(1024, dtype=torch.int32, device=dev)
-    krex.gen(w, cfg["seed"], 0)
-    cmds = W.mixed_stream_commands(w.cpu().numpy().view(np.uint32))
-    del x, y
-    xbuf = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
-    ybuf = torch.empty_like(xbuf)
-    tdt = {0: torch.float32, 1: torch.bfloat16, 2: torch.float16, 3: torch.float8_e4m3fn}
-    torch.cuda.synchronize()
-    kernel_ms, total = 0.0, 0
-    t0 = time.perf_counter()
-    for c in cmds:
-        xv = xbuf[:c.nbytes].view(tdt[c.dtype])
-        yv = ybuf[:c.nbytes].view(tdt[c.dtype])
-        e0 = ev()
-        # x and y in one pass (the same tensors as generation, then injection)
-        krex.gen_inject(xv, yv, c.value_seed, 0, c.dist, c.p0, c.p1, mask_seed=c.mask_seed, rate=c.rate,
-                        delta=cfg["delta"], mode="round")
-        krex.check(yv, xv, c.rtol, c.atol, out=res, sync=False)
-        krex.flush(fl512)
-        e1 = ev()
-        krex.decode_check_result(res)
-        kernel_ms += e0.elapsed_time(e1)
-        total += c.nbytes * 4 + cfg["flush_bytes"]
-    wall = time.perf_counter() - t0
-    out["commands"]["mixed_stream"] = {"GBps": round(total / (kernel_ms / 1e3) / 1e9, 1), "bytes": total,
-                                       "wall_GBps": round(total / wall / 1e9, 1),
-                                       "commands_per_s": round(len(cmds) / wall, 1)}
+    del A, B, C, Cref, fl512
+    out["commands"]["check_stress"] = measure_check_stress()
+    cmds, out["commands"]["mixed_stream"] = measure_mixed_stream()
     krex.detach()
     if with_cpu:
-        for k, v in configs_cpu_baseline(cmds).items():
-            out["commands"][k]["cpu_baseline"] = v
+        with pinned_core() as pc:
+            for k, v in configs_cpu_baseline(cmds).items():
+                v.update(host_facts())
+                v["core"] = pc.core
+                out["commands"][k]["cpu_baseline"] = v
     return out
+
+
+def run_hbm_commands():
+    """The two commands whose bytes are generation and check rather than
+    flush, at full size, attached and gated like any command:
+    check_stress (2 GiB of generation, injection and check) and
+    mixed_stream (64 commands, about 73 GB)."""
+    import torch
+
+    import paper_2609_30057_amd as krex
+    torch.cuda.set_device(0)
+    krex.attach(0, shm_name="/krex-hbm-%s" % uuid.uuid4().hex[:10])
+    try:
+        cs = measure_check_stress()
+        _, ms = measure_mixed_stream()
+    finally:
+        krex.detach()
+    return {"check_stress": cs, "mixed_stream": ms}
+
+
+def run_cache_probe(reps=11):
+    """What the cache flush must evict, measured: reads (torch's sum, ordinary
+    loads that allocate in the caches) of a 64 MiB buffer x timed with HIP
+    events in three states:
+      warm     x was read by the launch just before (it fits in the 256 MB
+               Infinity Cache);
+      flushed  a 1 GiB flush (k_flush) ran between the two reads;
+      cold     64 MiB slices of a 2 GiB buffer, written in order and then
+               read in order, so at least 1.9 GiB of other traffic separates
+               each slice's last touch from its read (no cache can hold it);
+    and, for the L2, a 2 MiB buffer read twice in a row (it fits in every
+    XCD's 4 MB L2): under `rocprofv3 --pmc TCC_HIT_sum TCC_MISS_sum` the
+    second read's hits show whether L2 contents survive a kernel boundary.
+    Each measured read is preceded by a one-iteration probe launch that marks
+    it in a kernel trace."""
+    import numpy as np
+    import torch
+
+    import paper_2609_30057_amd as krex
+    torch.cuda.set_device(0)
+    dev = "cuda:0"
+    x = torch.ones(16 << 20, dtype=torch.float32, device=dev)
+    fl = torch.empty(GIB // 4, dtype=torch.int32, device=dev)
+    W = torch.empty(32, 16 << 20, dtype=torch.float32, device=dev)
+    small = torch.ones(1 << 19, dtype=torch.float32, device=dev)
+    sink = torch.empty(krex.PROBE_THREADS, dtype=torch.float32, device=dev)
+
+    def timed(t):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        krex.probe(1, sink)
+        a.record()
+        t.sum()
+        b.record()
+        b.synchronize()
+        return a.elapsed_time(b)
+
+    for _ in range(5):
+        timed(x)
+    warm, flushed, cold = [], [], []
+    for _ in range(reps):
+        x.sum()
+        warm.append(timed(x))
+        krex.flush(fl, 7)
+        flushed.append(timed(x))
+    W.fill_(1.0)
+    for k in range(min(reps, 32)):
+        cold.append(timed(W[k]))
+    small.sum()
+    l2 = [timed(small) for _ in range(3)]
+    med = {k: float(np.median(v)) for k, v in (("warm", warm), ("flushed", flushed), ("cold", cold))}
+    mib = 64 * (1 << 20)
+    return {"metric": "64 MiB read time (ms) by cache state; GB/s", "reps": reps,
+            "ms": {k: round(v, 4) for k, v in med.items()},
+            "GBps": {k: round(mib / (v / 1e3) / 1e9, 1) for k, v in med.items()},
+            "flushed_over_cold": round(med["flushed"] / med["cold"], 3),
+            "warm_over_cold": round(med["warm"] / med["cold"], 3),
+            "l2_small_read_ms": [round(v, 4) for v in l2]}
 
 
 def run_copy_calibration():
@@ -542,11 +726,17 @@ def main():
     ap.add_argument("--siblings", type=int, default=None, help="fidelity sibling processes (default 7)")
     ap.add_argument("--warmup-ms", type=float, default=None,
                     help="fidelity: in-region warm-up time per sample (default 3 ms; 0: one warm-up launch)")
+    ap.add_argument("--warmup-mode", default="time", choices=("time", "clock"),
+                    help="fidelity: warm up by time, or until the probe's clock reaches its calibration median")
+    ap.add_argument("--sessions", type=int, default=1, help="fidelity: repeats of the compared modes")
+    ap.add_argument("--durations", default=None, help="fidelity: probe durations in ms, comma-separated")
     ap.add_argument("--modes", default=None,
                     help="fidelity modes, comma-separated from control,gated,ungated,frozen")
     ap.add_argument("--kernels", action="store_true")
     ap.add_argument("--calib-copy", action="store_true")
     ap.add_argument("--configs", action="store_true")
+    ap.add_argument("--cache-probe", action="store_true",
+                    help="64 MiB reads warm / after a 1 GiB flush / cold, and an L2 re-read (rocprofv3 --pmc)")
     ap.add_argument("--valu-rates", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -556,13 +746,18 @@ def main():
         from paper_2609_30057_amd import fidelity
         modes = args.modes.split(",") if args.modes else None
         print(json.dumps(fidelity.run(samples=args.samples, modes=modes, siblings=args.siblings,
-                                      warmup_ms=args.warmup_ms)), flush=True)
+                                      warmup_ms=args.warmup_ms, warmup=args.warmup_mode, sessions=args.sessions,
+                                      durations_ms=tuple(float(x) for x in args.durations.split(","))
+                                      if args.durations else None)), flush=True)
         return
     if args.kernels:
         out = run_kernels()
         if args.calib_copy:
             run_copy_calibration()
         print(json.dumps(out), flush=True)
+        return
+    if args.cache_probe:
+        print(json.dumps(run_cache_probe()), flush=True)
         return
     if args.configs:
         print(json.dumps(run_configs(not args.no_cpu_baseline)), flush=True)
@@ -574,6 +769,7 @@ def main():
             raise SystemExit("valu_rates is not built; run __graft_entry__.build()")
         sys.exit(subprocess.run([exe]).returncode)
     out = run_gemm_large(args.steps, args.warmup, not args.no_cpu_baseline)
+    out.update(run_hbm_commands())
     if args.calib_copy:
         run_copy_calibration()
     if not args.no_fidelity:

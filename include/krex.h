@@ -258,6 +258,17 @@ krex_status krex_flush(void *buf, uint64_t bytes, uint32_t pattern, void *stream
 #define KREX_PROBE_THREADS 65536
 krex_status krex_probe(uint64_t iters, float *sink, void *stream);
 
+/* krex_probe that also records each wave's clocks (the per-sample evidence
+ * of the device's clock state behind a timing ratio of Eq. 1): clocks
+ * (device, 16-byte aligned, KREX_PROBE_WAVES x 8 uint64 words) receives for
+ * wave w = 4 block + wave-in-block, at words 8w .. 8w + 7: the shader-clock
+ * cycle counter at the wave's start and end, the constant 100 MHz real-time
+ * counter at its start and end, the HW_ID register, 0, the XCC_ID register,
+ * 0. sink as for krex_probe, with the same values. */
+#define KREX_PROBE_WAVES 1024
+#define KREX_PROBE_CLOCK_WORDS 8
+krex_status krex_probe_clocked(uint64_t iters, float *sink, uint64_t *clocks, void *stream);
+
 /* --- critical region --------------------------------------------------------
  * Begins a critical region on this process's GPU (Section 4.1; Section 4.2):
  * waits for this process's own earlier GPU work, takes the region lock
@@ -304,6 +315,7 @@ krex_status krex_time_loop(krex_launch_fn fn, void *user, uint32_t warmup, uint3
 typedef struct krex_probe_args {
     uint64_t iters;
     float *sink;          /* device, KREX_PROBE_THREADS floats */
+    uint64_t *clocks;     /* NULL, or as for krex_probe_clocked */
 } krex_probe_args;
 void krex_probe_launch(void *user /* krex_probe_args* */, void *stream);
 

@@ -30,6 +30,8 @@ TL_REGION = 1
 ATTACH_NO_GATE = 1
 ATTACH_CPU_EXCLUSIVE = 2
 PROBE_THREADS = 65536
+PROBE_WAVES = 1024
+PROBE_CLOCK_WORDS = 8
 
 OK, RECOVERED = 0, 1
 EINVAL, EALIGN, EHIP, ETIMEDOUT, ESTATE, ENOTATTACHED, ENOMEM, EPEER, ESYS, EREVOKED = (
@@ -57,7 +59,7 @@ class _CheckResult(ctypes.Structure):
 
 
 class _ProbeArgs(ctypes.Structure):
-    _fields_ = [("iters", ctypes.c_uint64), ("sink", ctypes.c_void_p)]
+    _fields_ = [("iters", ctypes.c_uint64), ("sink", ctypes.c_void_p), ("clocks", ctypes.c_void_p)]
 
 
 class _SgemmArgs(ctypes.Structure):
@@ -117,6 +119,7 @@ def lib():
             "krex_check_gen_packed": (i32, [vp, i32, i32, u64, u64, u64, i32, f32, f32, f32, f32, vp, vp]),
             "krex_flush": (i32, [vp, u64, u32, vp]),
             "krex_probe": (i32, [u64, vp, vp]),
+            "krex_probe_clocked": (i32, [u64, vp, vp, vp]),
             "krex_region_begin": (i32, [vp, u32, vp, u64]),
             "krex_region_end": (i32, [vp]),
             "krex_time_loop": (i32, [LAUNCH_FN, vp, u32, u32, vp, u64, u32, u32, vp, vp, vp]),
@@ -340,10 +343,37 @@ def flush(buf, pattern=0, stream=None):
          "krex_flush")
 
 
-def probe(iters, sink, stream=None):
+def _check_clock_buffer(clocks):
+    t = _torch()
+    if clocks.dtype != t.int64 or clocks.numel() < PROBE_WAVES * PROBE_CLOCK_WORDS or not clocks.is_contiguous():
+        raise ValueError("clocks must be a contiguous int64 tensor of %d values" % (PROBE_WAVES * PROBE_CLOCK_WORDS))
+    if clocks.data_ptr() % 16:
+        raise ValueError("clocks must be 16-byte aligned")
+
+
+def probe(iters, sink, stream=None, clocks=None):
     if sink.numel() < PROBE_THREADS or sink.dtype != _torch().float32:
         raise ValueError("sink must hold %d float32 values" % PROBE_THREADS)
-    _chk(lib().krex_probe(iters, _dev(sink), _stream(stream)), "krex_probe")
+    if clocks is None:
+        _chk(lib().krex_probe(iters, _dev(sink), _stream(stream)), "krex_probe")
+    else:
+        _check_clock_buffer(clocks)
+        _chk(lib().krex_probe_clocked(iters, _dev(sink), _dev(clocks), _stream(stream)), "krex_probe_clocked")
+
+
+def probe_clocks(clocks):
+    """Decodes one probe's clock record (a tensor filled by probe(...,
+    clocks=) or a clocked probe_launcher) into numpy arrays per wave:
+    cycles and real-time ticks (100 MHz) elapsed, the effective shader clock
+    in MHz, the start and end real-time stamps, the XCD and the HW_ID."""
+    import numpy as np
+    a = clocks[:PROBE_WAVES * PROBE_CLOCK_WORDS].cpu().numpy().view(np.uint64).reshape(PROBE_WAVES, PROBE_CLOCK_WORDS)
+    cyc = (a[:, 1] - a[:, 0]).astype(np.float64)
+    rt = (a[:, 3] - a[:, 2]).astype(np.float64)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        mhz = np.where(rt > 0, cyc / rt * 100.0, np.nan)
+    return {"cycles": cyc, "rt_ticks": rt, "mhz": mhz, "rt_start": a[:, 2], "rt_end": a[:, 3],
+            "xcc": (a[:, 6] & 0xF).astype(np.int64), "hw_id": a[:, 4].astype(np.int64)}
 
 
 def fixture_sgemm(A, B, C, stream=None):
@@ -408,9 +438,13 @@ def gate_stats():
 
 # --------------------------------------------------------------------- timed loop
 
-def probe_launcher(iters, sink):
-    """(fn, user) for time_loop that launches the probe kernel from C."""
-    args = _ProbeArgs(iters, _dev(sink))
+def probe_launcher(iters, sink, clocks=None):
+    """(fn, user) for time_loop that launches the probe kernel from C;
+    clocks: None or a device tensor of PROBE_WAVES * PROBE_CLOCK_WORDS int64
+    (see probe_clocks)."""
+    if clocks is not None:
+        _check_clock_buffer(clocks)
+    args = _ProbeArgs(iters, _dev(sink), _dev(clocks) if clocks is not None else None)
     fn = ctypes.cast(ctypes.cast(lib().krex_probe_launch, ctypes.c_void_p).value, LAUNCH_FN)
     return fn, args
 

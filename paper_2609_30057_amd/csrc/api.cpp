@@ -509,7 +509,15 @@ krex_status krex_probe(uint64_t iters, float *sink, void *stream)
     if (!sink) return KREX_EINVAL;
     if (!aligned(sink, 4)) return KREX_EALIGN;
     hipStream_t s = (hipStream_t)stream;
-    return submit(s, [&] { return krex::launch_probe(iters, sink, s); });
+    return submit(s, [&] { return krex::launch_probe(iters, sink, nullptr, s); });
+}
+
+krex_status krex_probe_clocked(uint64_t iters, float *sink, uint64_t *clocks, void *stream)
+{
+    if (!sink || !clocks) return KREX_EINVAL;
+    if (!aligned(sink, 4) || !aligned(clocks, 16)) return KREX_EALIGN;
+    hipStream_t s = (hipStream_t)stream;
+    return submit(s, [&] { return krex::launch_probe(iters, sink, clocks, s); });
 }
 
 krex_status krex_fixture_sgemm(uint32_t M, uint32_t N, uint32_t K, const float *A, const float *B, float *C,
@@ -524,7 +532,7 @@ krex_status krex_fixture_sgemm(uint32_t M, uint32_t N, uint32_t K, const float *
 void krex_probe_launch(void *user, void *stream)
 {
     const krex_probe_args *a = (const krex_probe_args *)user;
-    const hipError_t e = krex::launch_probe(a->iters, a->sink, (hipStream_t)stream);
+    const hipError_t e = krex::launch_probe(a->iters, a->sink, a->clocks, (hipStream_t)stream);
     if (e != hipSuccess && g_fn_error == hipSuccess) g_fn_error = e;
 }
 

@@ -1018,9 +1018,22 @@ hipError_t launch_flush(void *buf, uint64_t bytes, uint32_t pattern, hipStream_t
 
 // ---------------------------------------------------------------------- probe
 
-__global__ __launch_bounds__(kThreads) void k_probe(uint64_t iters, float *sink)
+// clocks (optional): per wave w = 4 blockIdx.x + wave, eight 64-bit words
+// at clocks + 8 w: the shader-clock cycle counter (s_memtime) and the
+// constant-rate real-time counter (s_memrealtime, 100 MHz) read when the
+// wave starts and when its chains are done, the HW_ID register (CU, SIMD,
+// shader array / engine) and the XCC_ID register. The wave's
+// effective shader clock is its cycle delta over its real-time delta. Only
+// the wave's first lane stores, with an ordinary vector store; the sink's
+// value does not depend on it.
+__global__ __launch_bounds__(kThreads) void k_probe(uint64_t iters, float *sink, uint64_t *clocks)
 {
     const uint32_t g = blockIdx.x * kThreads + threadIdx.x;
+    uint64_t c0 = 0, r0 = 0;
+    if (clocks) {
+        c0 = __builtin_amdgcn_s_memtime();
+        r0 = __builtin_amdgcn_s_memrealtime();
+    }
     float x[8];
 #pragma unroll
     for (int c = 0; c < 8; ++c) x[c] = (float)(g * 8u + (uint32_t)c) * 0x1p-19f;
@@ -1033,12 +1046,28 @@ __global__ __launch_bounds__(kThreads) void k_probe(uint64_t iters, float *sink)
     float s = x[0];
 #pragma unroll
     for (int c = 1; c < 8; ++c) s = s + x[c];
+    if (clocks) {
+        // the end stamps depend on s, so they are read after the chains
+        __asm__ volatile("" ::"v"(s));
+        const uint64_t c1 = __builtin_amdgcn_s_memtime();
+        const uint64_t r1 = __builtin_amdgcn_s_memrealtime();
+        uint32_t hw, xcc;
+        __asm__ volatile("s_getreg_b32 %0, hwreg(HW_REG_HW_ID)" : "=s"(hw));
+        __asm__ volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+        if ((threadIdx.x & 63u) == 0) {
+            uint4 *o = reinterpret_cast<uint4 *>(clocks + 8u * (blockIdx.x * (kThreads / 64) + threadIdx.x / 64));
+            o[0] = make_uint4((uint32_t)c0, (uint32_t)(c0 >> 32), (uint32_t)c1, (uint32_t)(c1 >> 32));
+            o[1] = make_uint4((uint32_t)r0, (uint32_t)(r0 >> 32), (uint32_t)r1, (uint32_t)(r1 >> 32));
+            o[2] = make_uint4(hw, 0u, xcc, 0u);
+            o[3] = make_uint4(0u, 0u, 0u, 0u);
+        }
+    }
     sink[g] = s;
 }
 
-hipError_t launch_probe(uint64_t iters, float *sink, hipStream_t s)
+hipError_t launch_probe(uint64_t iters, float *sink, uint64_t *clocks, hipStream_t s)
 {
-    return launch(k_probe, dim3(256), dim3(kThreads), s, iters, sink);
+    return launch(k_probe, dim3(kProbeBlocks), dim3(kThreads), s, iters, sink, clocks);
 }
 
 // ------------------------------------------------------------------- fixture

@@ -62,7 +62,10 @@ hipError_t launch_check_gen_packed(const void *a, int dta, int dtb, uint64_t n, 
                                    int dist, float p0, float p1, float rtol, float atol, void *scratch,
                                    krex_check_result *out, hipStream_t s);
 hipError_t launch_flush(void *buf, uint64_t bytes, uint32_t pattern, hipStream_t s);
-hipError_t launch_probe(uint64_t iters, float *sink, hipStream_t s);
+// The probe: kProbeBlocks blocks of 256 threads; clocks (device,
+// 8 x 64-bit words per wave, kProbeBlocks x 4 waves) or null.
+static constexpr int kProbeBlocks = 256;
+hipError_t launch_probe(uint64_t iters, float *sink, uint64_t *clocks, hipStream_t s);
 hipError_t launch_sgemm(uint32_t M, uint32_t N, uint32_t K, const float *A, const float *B, float *C,
                         hipStream_t s);
 

@@ -119,33 +119,91 @@ def _settle(krex, sink, seconds):
 
 
 def _calibrate(krex, sink, target_ms):
+    """Iterations for a probe of about target_ms alone; returns (iters, median
+    ms, median wave clock in MHz of the last calibration launches)."""
+    import torch
     iters = 20000
     for _ in range(4):
         t = float(np.median(krex.time_loop(krex.probe_launcher(iters, sink), 2, 7)))
         iters = max(1, int(round(iters * target_ms / t)))
-    t = float(np.median(krex.time_loop(krex.probe_launcher(iters, sink), 2, 7)))
-    return iters, t
+    clk = torch.zeros(krex.PROBE_WAVES * krex.PROBE_CLOCK_WORDS, dtype=torch.int64, device="cuda:0")
+    ts, mhz = [], []
+    for _ in range(7):
+        ts.append(krex.time_loop(krex.probe_launcher(iters, sink, clk), 2, 1)[0])
+        mhz.append(float(np.nanmedian(krex.probe_clocks(clk)["mhz"])))
+    return iters, float(np.median(ts)), float(np.median(mhz))
 
 
-def _measure(krex, plan, samples, fl, sink, gap_ms, warmup_ms=0.0):
-    """warmup_ms > 0: warm-up launches inside the region until about that
-    long (so the device's clocks settle after the siblings stop), instead of
-    a single one."""
-    times, drains = {}, []
+def clock_summary(clk):
+    """Per-sample clock figures from a (samples, PROBE_WAVES * 8) int64 tensor
+    of probe clock records: the median and minimum of the waves' effective
+    shader clocks (MHz), and the real-time span of the launch (first wave
+    start to last wave end, ms)."""
+    a = clk.cpu().numpy().view(np.uint64).reshape(clk.shape[0], -1, 8)
+    cyc = (a[:, :, 1] - a[:, :, 0]).astype(np.float64)
+    rt = (a[:, :, 3] - a[:, :, 2]).astype(np.float64)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        mhz = np.where(rt > 0, cyc / rt * 100.0, np.nan)
+    span = (a[:, :, 3].max(axis=1) - a[:, :, 2].min(axis=1)).astype(np.float64) / 1e5
+    return {"mhz_med": np.nanmedian(mhz, axis=1), "mhz_min": np.nanmin(mhz, axis=1), "span_ms": span}
+
+
+def _measure(krex, plan, samples, fl, sink, gap_ms, warmup_ms=0.0, warm_clock=None):
+    """Single-shot samples of each (duration, iters) of `plan`, each in its
+    own region. warmup_ms > 0: warm-up launches inside the region for about
+    that long before the flush and the timed launch (so the device's clocks
+    settle after the siblings stop); 0: one warm-up launch. warm_clock =
+    (target_mhz, cap_ms): instead, warm-up launches one at a time, each
+    followed by a read of its clock record, until the median wave clock
+    reaches target_mhz (at least one launch; stop after cap_ms). Every timed
+    launch records its clocks. Returns times, drains, clock summaries and
+    warm-up launch counts per duration."""
+    import torch
+    times, drains, clocks, warms = {}, [], {}, {}
+    words = krex.PROBE_WAVES * krex.PROBE_CLOCK_WORDS
     for d, iters in plan:
-        fn = krex.probe_launcher(iters, sink)
+        clk = torch.zeros((samples, words), dtype=torch.int64, device="cuda:0")
+        wclk = torch.zeros(words, dtype=torch.int64, device="cuda:0")
         warm = max(1, int(round(warmup_ms / d))) if warmup_ms > 0 else 1
-        ts = []
-        for _ in range(samples):
-            ts.append(krex.time_loop(fn, warm, 1, flush_buf=fl, region=True)[0])
+        wfn = krex.probe_launcher(iters, sink, wclk)
+        ts, nw = [], []
+        for i in range(samples):
+            fn = krex.probe_launcher(iters, sink, clk[i])
+            if warm_clock is None:
+                ts.append(krex.time_loop(fn, warm, 1, flush_buf=fl, region=True)[0])
+                nw.append(warm)
+            else:
+                target, cap_ms = warm_clock
+                krex.region_begin()
+                try:
+                    n, t0 = 0, time.perf_counter()
+                    while True:
+                        krex.time_loop(wfn, 0, 1)          # one launch, synchronised
+                        n += 1
+                        mhz = float(np.nanmedian(krex.probe_clocks(wclk)["mhz"]))
+                        if mhz >= target or (time.perf_counter() - t0) * 1e3 >= cap_ms:
+                            break
+                    ts.append(krex.time_loop(fn, 0, 1, flush_buf=fl)[0])
+                finally:
+                    krex.region_end()
+                nw.append(n)
             drains.append(krex.gate_stats()["last_drain_ns"] / 1e6)
             time.sleep(gap_ms / 1e3)
         times[d] = ts
-    return times, drains
+        clocks[d] = clock_summary(clk)
+        warms[d] = nw
+        del clk
+    return times, drains, clocks, warms
 
 
 def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, modes=None, warmup_ms=None,
-        settle_s=2.0):
+        settle_s=2.0, warmup="time", sessions=1, clock_cap_ms=20.0):
+    """warmup: "time" (launches for about warmup_ms in each region) or
+    "clock" (launches until the probe's clock reaches the calibration
+    median, at most clock_cap_ms), the same procedure for every mode, the
+    native run included. sessions: how many times the compared modes are
+    measured in turn after the native run (P per session in P_sessions; P is
+    the first session's)."""
     import torch
 
     import paper_2609_30057_amd as krex
@@ -155,6 +213,8 @@ def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, mode
     durations_ms = durations_ms or cfg["probe_ms"]
     siblings = cfg["siblings"] if siblings is None else siblings
     n = sibling_elems or W.CHECK_STRESS["rows"] * W.CHECK_STRESS["cols"]
+    if warmup not in ("time", "clock"):
+        raise ValueError("warmup is 'time' or 'clock'")
     torch.cuda.set_device(0)
     fl = torch.empty(cfg["flush_bytes"] // 4, dtype=torch.int32, device="cuda:0")
     sink = torch.empty(krex.PROBE_THREADS, dtype=torch.float32, device="cuda:0")
@@ -163,11 +223,14 @@ def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, mode
               "siblings": siblings, "sibling_workload": "check_stress gen+inject+check, %d fp16 elements" % n,
               "flush_bytes": cfg["flush_bytes"], "gap_ms": cfg["gap_ms"], "P": {}, "P_median_of_10": {},
               "median_ratio": {}, "within_5pct": {}, "calibrated": {}, "sibling_GBps": {}, "drain_ms": {},
-              "warmup_ms": warmup_ms}
-    times = {}
+              "warmup": warmup, "warmup_ms": warmup_ms if warmup == "time" else None,
+              "clock_cap_ms": clock_cap_ms if warmup == "clock" else None, "sessions": sessions}
+    times, clocks, warms = {}, {}, {}
     modes = list(modes or ("native", "control", "gated", "ungated"))
     compared = [m for m in modes if m != "native"]
-    for mode in ["native"] + compared:
+    runs = [("native", 0)] + [(m, k) for k in range(sessions) for m in compared]
+    plan, targets = [], {}
+    for mode, sess in runs:
         gated = mode not in ("ungated", "torch_ungated")
         shm = "/krex-fid-%s" % uuid.uuid4().hex[:10]
         frozen = mode in ("frozen", "frozen_nopin")
@@ -178,11 +241,11 @@ def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, mode
         krex.attach(0, shm_name=shm, gated=gated, cpu_exclusive=frozen)
         if mode == "native":
             _settle(krex, sink, settle_s)
-            plan = []
             for d in durations_ms:
-                iters, t = _calibrate(krex, sink, d)
+                iters, t, mhz = _calibrate(krex, sink, d)
                 plan.append((d, iters))
-                result["calibrated"][str(d)] = {"iters": iters, "ms": round(t, 4)}
+                targets[d] = mhz
+                result["calibrated"][str(d)] = {"iters": iters, "ms": round(t, 4), "clock_MHz": round(mhz, 1)}
         procs, stop, q = [], ctx.Event(), ctx.Queue()
         torch_procs, stop_path = [], None
         if mode in ("torch_gated", "torch_ungated"):
@@ -200,8 +263,18 @@ def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, mode
                 if not r.wait(600):
                     raise RuntimeError("sibling did not start")
         t0 = time.perf_counter()
-        times[mode], drains = _measure(krex, plan, samples, fl, sink, cfg["gap_ms"], warmup_ms)
+        key = (mode, sess)
+        tm, drains, ck, wm = {}, [], {}, {}
+        for d, iters in plan:
+            wc = (targets[d], clock_cap_ms) if warmup == "clock" else None
+            a, b, c, e = _measure(krex, [(d, iters)], samples, fl, sink, cfg["gap_ms"], warmup_ms, wc)
+            tm.update(a)
+            drains += b
+            ck.update(c)
+            wm.update(e)
+        times[key], clocks[key], warms[key] = tm, ck, wm
         wall = time.perf_counter() - t0
+        tag = mode if sess == 0 else "%s#%d" % (mode, sess)
         if torch_procs:
             open(stop_path, "w").close()
             rounds, secs = 0, 0.0
@@ -211,7 +284,7 @@ def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, mode
                 rounds += int(last[1])
                 secs = max(secs, float(last[2]))
             os.unlink(stop_path)
-            result.setdefault("torch_sibling_TFLOPs", {})[mode] = round(rounds * 2 * 4096**3 / secs / 1e12, 1)
+            result.setdefault("torch_sibling_TFLOPs", {})[tag] = round(rounds * 2 * 4096**3 / secs / 1e12, 1)
         if procs:
             stop.set()
             got = [q.get(timeout=300) for _ in procs]
@@ -219,29 +292,51 @@ def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, mode
                 p.join(120)
             rounds = sum(g[0] for g in got)
             secs = max(g[1] for g in got)
-            result["sibling_GBps"][mode] = round(rounds * 10 * n / secs / 1e9, 1)
-            result["sibling_parks"] = result.get("sibling_parks", {})
-            result["sibling_parks"][mode] = int(sum(g[2]["parks"] for g in got))
-        d = np.asarray(drains)
-        result["drain_ms"][mode] = {"p50": round(float(np.median(d)), 4), "p95": round(float(np.percentile(d, 95)), 4),
-                                    "max": round(float(d.max()), 4)}
-        result.setdefault("wall_s", {})[mode] = round(wall, 1)
+            result["sibling_GBps"][tag] = round(rounds * 10 * n / secs / 1e9, 1)
+            result.setdefault("sibling_parks", {})[tag] = int(sum(g[2]["parks"] for g in got))
+        dd = np.asarray(drains)
+        result["drain_ms"][tag] = {"p50": round(float(np.median(dd)), 4), "p95": round(float(np.percentile(dd, 95)), 4),
+                                   "max": round(float(dd.max()), 4)}
+        result.setdefault("wall_s", {})[tag] = round(wall, 1)
         krex.detach()
-        print("fidelity: %s done (%.1f s)" % (mode, wall), file=sys.stderr, flush=True)
+        print("fidelity: %s done (%.1f s)" % (tag, wall), file=sys.stderr, flush=True)
+    nat = ("native", 0)
     for d in durations_ms:
-        native = float(np.median(times["native"][d]))
+        native = float(np.median(times[nat][d]))
+        nat_mhz = float(np.median(clocks[nat][d]["mhz_med"]))
         key = str(d)
-        result["P"][key] = {m: round(100 * stats.p95_inflation(times[m][d], native), 3)
-                            for m in compared}
-        nat10 = float(np.median(stats.medians_of(times["native"][d])))
-        result["P_median_of_10"][key] = {m: round(100 * stats.p95_inflation(stats.medians_of(times[m][d]), nat10), 3)
-                                         for m in compared}
-        result["median_ratio"][key] = {m: round(stats.median_ratio(times[m][d], native), 4)
-                                       for m in compared}
-        result["within_5pct"][key] = {m: round(stats.within(times[m][d], native), 4)
-                                      for m in compared}
+        first = {m: (m, 0) for m in compared}
+        result["P"][key] = {m: round(100 * stats.p95_inflation(times[k][d], native), 3) for m, k in first.items()}
+        if sessions > 1:
+            result.setdefault("P_sessions", {})[key] = {
+                m: [round(100 * stats.p95_inflation(times[(m, s)][d], native), 3) for s in range(sessions)]
+                for m in compared}
+        nat10 = float(np.median(stats.medians_of(times[nat][d])))
+        result["P_median_of_10"][key] = {m: round(100 * stats.p95_inflation(stats.medians_of(times[k][d]), nat10), 3)
+                                         for m, k in first.items()}
+        result["median_ratio"][key] = {m: round(stats.median_ratio(times[k][d], native), 4)
+                                       for m, k in first.items()}
+        result["within_5pct"][key] = {m: round(stats.within(times[k][d], native), 4) for m, k in first.items()}
         result["calibrated"][key]["native_median_ms"] = round(native, 4)
         result.setdefault("ratio_quantiles", {})[key] = {
-            m: [round(float(q), 4) for q in np.percentile(np.asarray(times[m][d]) / native, [5, 50, 90, 95, 99, 100])]
-            for m in ["native"] + compared}
+            m: [round(float(q), 4) for q in np.percentile(np.asarray(times[k][d]) / native, [5, 50, 90, 95, 99, 100])]
+            for m, k in [("native", nat)] + list(first.items())}
+        # Clock evidence per sample: each timed launch's median wave clock.
+        # clock_corrected: the sample's time scaled to the native run's
+        # median clock (t f / f_native), i.e. what is left once the clock
+        # difference is taken out.
+        cl = {}
+        for m, k in [("native", nat)] + list(first.items()):
+            t = np.asarray(times[k][d])
+            f = clocks[k][d]["mhz_med"]
+            r = t / native
+            ok = np.isfinite(f)
+            corr = float(np.corrcoef(r[ok], nat_mhz / f[ok])[0, 1]) if ok.sum() > 2 and np.std(f[ok]) > 0 else None
+            cl[m] = {"MHz_p5_p50_p95": [round(float(v), 1) for v in np.nanpercentile(f, [5, 50, 95])],
+                     "MHz_min_wave_p5": round(float(np.nanpercentile(clocks[k][d]["mhz_min"], 5)), 1),
+                     "corr_ratio_vs_clock_deficit": None if corr is None else round(corr, 3),
+                     "P_clock_corrected": round(100 * stats.p95_inflation(t[ok] * f[ok] / nat_mhz, native), 3),
+                     "warmup_launches_p50_p95": [int(np.median(warms[k][d])),
+                                                 int(np.percentile(warms[k][d], 95))]}
+        result.setdefault("clock", {})[key] = cl
     return result

@@ -66,6 +66,7 @@ def test_constants_match_binding():
              "KREX_ATTACH_NO_GATE": k.ATTACH_NO_GATE,
              "KREX_ATTACH_CPU_EXCLUSIVE": k.ATTACH_CPU_EXCLUSIVE,
              "KREX_EREVOKED": k.EREVOKED, "KREX_PROBE_THREADS": k.PROBE_THREADS,
+             "KREX_PROBE_WAVES": k.PROBE_WAVES, "KREX_PROBE_CLOCK_WORDS": k.PROBE_CLOCK_WORDS,
              "KREX_OK": k.OK, "KREX_RECOVERED": k.RECOVERED, "KREX_EINVAL": k.EINVAL, "KREX_EALIGN": k.EALIGN,
              "KREX_EHIP": k.EHIP, "KREX_ETIMEDOUT": k.ETIMEDOUT, "KREX_ESTATE": k.ESTATE,
              "KREX_ENOTATTACHED": k.ENOTATTACHED, "KREX_ENOMEM": k.ENOMEM, "KREX_EPEER": k.EPEER,
@@ -120,6 +121,11 @@ def test_host_only_entry_points():
                                    ctypes.c_void_p(8), None) == k.EALIGN
     assert L.krex_inject(None, None, k.F16, 4, 0, 0, 1.5, 0.5, 1, None) == k.EINVAL
     assert L.krex_flush(None, 17, 0, None) == k.EINVAL
+    assert L.krex_probe_clocked(10, ctypes.c_void_p(16), None, None) == k.EINVAL
+    assert L.krex_probe_clocked(10, ctypes.c_void_p(16), ctypes.c_void_p(8), None) == k.EALIGN
+    assert L.krex_check_noalloc(None, k.F32, None, k.F32, 2**33, 0.0, 0.0, ctypes.c_void_p(8), None) == k.EINVAL
+    assert L.krex_check_noalloc(ctypes.c_void_p(16), k.F32, ctypes.c_void_p(16), k.F32, 4, 0.0, 0.0,
+                                ctypes.c_void_p(12), None) == k.EALIGN
     assert L.krex_region_begin(None, 10, None, 0) == k.ENOTATTACHED
     assert L.krex_region_end(None) == k.ENOTATTACHED
     assert L.krex_detach() == k.ESTATE
