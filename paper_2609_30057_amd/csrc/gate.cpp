@@ -26,6 +26,33 @@
 #include "krex.h"
 
 namespace krexg {
+// ThreadSanitizer builds of the CPU test harness: the sanitizer has no
+// interceptor for pthread_mutex_clocklock, so the acquisition is announced to
+// it explicitly (otherwise the matching unlock reads as an unlock of an
+// unlocked mutex). Other builds call the function directly.
+#if defined(__SANITIZE_THREAD__)
+#include <sanitizer/tsan_interface.h>
+#endif
+
+namespace {
+
+int timed_lock(pthread_mutex_t *m, const timespec *abs)
+{
+#if defined(__SANITIZE_THREAD__)
+    __tsan_mutex_pre_lock(m, 0);
+    const int rc = pthread_mutex_clocklock(m, CLOCK_MONOTONIC, abs);
+    if (rc == 0 || rc == EOWNERDEAD)
+        __tsan_mutex_post_lock(m, 0, 0);
+    else
+        __tsan_mutex_post_lock(m, __tsan_mutex_try_lock_failed, 0);
+    return rc;
+#else
+    return pthread_mutex_clocklock(m, CLOCK_MONOTONIC, abs);
+#endif
+}
+
+}  // namespace
+
 namespace {
 
 constexpr uint64_t kMagic = 0x4b52455847415445ull;   // "KREXGATE"
@@ -63,7 +90,8 @@ struct State {
     Segment *seg = nullptr;
     int slot = -1;
     bool gated_ = false;
-    bool in_region = false;
+    std::atomic<bool> in_region{false};
+    bool entering = false;             // a region_begin of this process waits for the region lock
     uint32_t flags = 0;
     uint32_t spin_us = 50;
     uint64_t region_gate = 0;          // gate word of this process's current region
@@ -469,7 +497,7 @@ int detach()
     State &s = st();
     std::lock_guard<std::mutex> g(s.mu);
     if (!s.seg) return KREX_ESTATE;
-    if (s.in_region) return KREX_ESTATE;
+    if (s.in_region || s.entering) return KREX_ESTATE;
     Segment *seg = s.seg;
     seg->slots[s.slot].inflight.store(0);
     seg->slots[s.slot].pid.store(0);
@@ -596,10 +624,18 @@ void release(uint64_t k)
 int region_begin(uint32_t timeout_ms)
 {
     State &s = st();
-    std::lock_guard<std::mutex> g(s.mu);
-    Segment *seg = s.seg;
-    if (!seg) return KREX_ENOTATTACHED;
-    if (s.in_region) return KREX_ESTATE;
+    Segment *seg = nullptr;
+    {
+        // The state is checked under the process mutex, but the wait for the
+        // region lock happens without it: the region lock always comes first
+        // (region_end holds it when it takes the mutex). `entering` keeps
+        // the other calls of this process out meanwhile.
+        std::lock_guard<std::mutex> g(s.mu);
+        seg = s.seg;
+        if (!seg) return KREX_ENOTATTACHED;
+        if (s.in_region || s.entering) return KREX_ESTATE;
+        s.entering = true;
+    }
     const uint64_t t0 = now_ns();
     const uint64_t deadline = t0 + (uint64_t)timeout_ms * 1000000ull;
     timespec abs;
@@ -612,7 +648,9 @@ int region_begin(uint32_t timeout_ms)
     }
     int status = KREX_OK;
     // Step 1: the region lock.
-    int rc = pthread_mutex_clocklock(&seg->lock, CLOCK_MONOTONIC, &abs);
+    int rc = timed_lock(&seg->lock, &abs);
+    std::lock_guard<std::mutex> g(s.mu);
+    s.entering = false;
     if (rc == EOWNERDEAD) {
         recover_dead_holder(seg);
         pthread_mutex_consistent(&seg->lock);

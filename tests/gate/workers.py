@@ -1,6 +1,7 @@
 """Process bodies for the region-coordinator tests (spawned, so each has its
 own copy of the coordinator's process state)."""
 import ctypes
+import os
 import time
 
 from tests.gate import harness
@@ -9,7 +10,10 @@ OK = 0
 
 
 def _L(variant=""):
-    return harness.load(variant)
+    # KREX_GATE_VARIANT selects the build for every worker of a test run
+    # (the ThreadSanitizer variant is loaded under libtsan, preloaded by the
+    # test that spawns these processes)
+    return harness.load(variant or os.environ.get("KREX_GATE_VARIANT", ""))
 
 
 def sibling_loop(name, dur_us, seconds, depth, q, variant=""):
@@ -220,3 +224,11 @@ def submit_twice(name, ready2, q):
     L.kg_wait_idle(10000)
     q.put(("sib", rc, t1, rc2, t2, harness.stats(L)))
     L.kg_detach()
+
+
+def report_loaded(q):
+    """Which coordinator build and sanitizer runtime this process mapped."""
+    _L()
+    with open("/proc/self/maps") as f:
+        maps = f.read()
+    q.put(("loaded", "libtsan" in maps, "libgate_harness_tsan.so" in maps))
