@@ -446,18 +446,21 @@ def _rate(nbytes, ms):
     return {"ms": round(ms, 4), "GBps": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 3)}
 
 
-def measure_check_stress(reps=5):
+def measure_check_stress(reps=5, per_kernel=5):
     """The check_stress command at full size (x fp16 16384 x 16384 uniform
     [-4, 4), seed 2; y = EXACT inject(x, mask seed 3, rate 0.001, delta 0.5);
     check(y, x) at rtol = atol = 1e-3), `reps` times each way: generation,
     injection and check as three launches, and generation with injection
-    fused (x and y written in one pass) followed by the check. HIP events on
-    the launching stream around each launch, about 0.1 ms of the probe
-    kernel ahead of the first event so no event times the host's enqueue;
-    medians over the reps. Algorithmic bytes (the method's): generation and
-    injection each write 2n, the check reads 4n, 8n = 2 GiB per command
-    either way; each kernel's fraction of 8 TB/s counts the bytes it moves
-    (injection: x read and y written, 4n)."""
+    fused (x and y written in one pass) followed by the check. The command's
+    time is HIP events around each step's launches, about 0.1 ms of the
+    probe kernel ahead of the first event so no event times the host's
+    enqueue; medians over the reps. Each kernel's own time is `per_kernel`
+    back-to-back launches of it between two events, divided by their count
+    (the launch gaps the step figures include are spread over them), median
+    over the reps: the figure a kernel trace reports. Algorithmic bytes (the
+    method's): generation and injection each write 2n, the check reads 4n,
+    8n = 2 GiB per command either way; each kernel's fraction of 8 TB/s counts
+    the bytes it moves (injection: x read and y written, 4n)."""
     import numpy as np
     import torch
 
@@ -471,30 +474,55 @@ def measure_check_stress(reps=5):
     y = torch.empty_like(x)
     res = krex.check_result_buffer(dev)
     lead = torch.empty(krex.PROBE_THREADS, dtype=torch.float32, device=dev)
-    sep, fus, verdicts = [], [], []
+
+    def gen():
+        krex.gen(x, cfg["seed"], 0, "uniform", cfg["p0"], cfg["p1"])
+
+    def inject():
+        krex.inject(y, x, cfg["mask_seed"], cfg["rate"], cfg["delta"], "exact")
+
+    def check():
+        krex.check(y, x, cfg["rtol"], cfg["atol"], out=res, sync=False)
+
+    def gen_inject():
+        krex.gen_inject(x, y, cfg["seed"], 0, "uniform", cfg["p0"], cfg["p1"], mask_seed=cfg["mask_seed"],
+                        rate=cfg["rate"], delta=cfg["delta"], mode="exact")
+
+    def per_launch(fn):
+        krex.probe(LEAD_PROBE_ITERS, lead)
+        a = _event()
+        for _ in range(per_kernel):
+            fn()
+        b = _event()
+        b.synchronize()
+        return a.elapsed_time(b) / per_kernel
+
+    sep, fus, verdicts, kern = [], [], [], {"gen": [], "inject": [], "check": [], "gen_inject": []}
     for _ in range(reps):
         krex.probe(LEAD_PROBE_ITERS, lead)
         e0 = _event()
-        krex.gen(x, cfg["seed"], 0, "uniform", cfg["p0"], cfg["p1"])
+        gen()
         e1 = _event()
-        krex.inject(y, x, cfg["mask_seed"], cfg["rate"], cfg["delta"], "exact")
+        inject()
         e2 = _event()
-        krex.check(y, x, cfg["rtol"], cfg["atol"], out=res, sync=False)
+        check()
         e3 = _event()
         v = krex.decode_check_result(res)
         sep.append((e0.elapsed_time(e1), e1.elapsed_time(e2), e2.elapsed_time(e3)))
         krex.probe(LEAD_PROBE_ITERS, lead)
         f0 = _event()
-        krex.gen_inject(x, y, cfg["seed"], 0, "uniform", cfg["p0"], cfg["p1"], mask_seed=cfg["mask_seed"],
-                        rate=cfg["rate"], delta=cfg["delta"], mode="exact")
+        gen_inject()
         f1 = _event()
-        krex.check(y, x, cfg["rtol"], cfg["atol"], out=res, sync=False)
+        check()
         f2 = _event()
         vf = krex.decode_check_result(res)
         fus.append((f0.elapsed_time(f1), f1.elapsed_time(f2)))
         verdicts.append((v, vf))
+        for name, fn in (("gen", gen), ("inject", inject), ("gen_inject", gen_inject), ("check", check)):
+            kern[name].append(per_launch(fn))
     tg, ti, tc = (float(np.median([r[k] for r in sep])) for k in range(3))
     tf, tcf = (float(np.median([r[k] for r in fus])) for k in range(2))
+    kt = {k: float(np.median(v)) for k, v in kern.items()}
     v, vf = verdicts[-1]
     same = all((a.mismatches, a.nan_count, a.argmax_abs, a.max_abs, a.max_rel)
                == (b.mismatches, b.nan_count, b.argmax_abs, b.max_abs, b.max_rel)
@@ -505,11 +533,12 @@ def measure_check_stress(reps=5):
                      "rate 0.001, delta 0.5); check(y, x) rtol 1e-3 atol 1e-3"),
         "algorithmic_bytes": alg,
         "reps": reps,
-        "separate": dict(_rate(alg, tg + ti + tc), kernels={
-            "gen_f16_uniform": _rate(2 * m, tg), "inject_f16_exact": _rate(4 * m, ti),
-            "check_f16_f16": _rate(4 * m, tc)}),
-        "fused": dict(_rate(alg, tf + tcf), kernels={
-            "gen_inject_f16": _rate(4 * m, tf), "check_f16_f16": _rate(4 * m, tcf)}),
+        "separate": dict(_rate(alg, tg + ti + tc), steps_ms=[round(tg, 4), round(ti, 4), round(tc, 4)]),
+        "fused": dict(_rate(alg, tf + tcf), steps_ms=[round(tf, 4), round(tcf, 4)]),
+        "kernels": {"gen_f16_uniform": _rate(2 * m, kt["gen"]), "inject_f16_exact": _rate(4 * m, kt["inject"]),
+                    "gen_inject_f16": _rate(4 * m, kt["gen_inject"]),
+                    "check_f16_f16 (+ final)": _rate(4 * m, kt["check"])},
+        "kernels_basis": "%d back-to-back launches between two events, per launch, median of %d" % (per_kernel, reps),
         "verdict": {"mismatches": v.mismatches, "nan_count": v.nan_count, "argmax_abs": v.argmax_abs,
                     "max_abs": v.max_abs, "max_rel": v.max_rel},
         "verdict_same_every_rep_and_path": bool(same),
@@ -726,9 +755,11 @@ def main():
     ap.add_argument("--siblings", type=int, default=None, help="fidelity sibling processes (default 7)")
     ap.add_argument("--warmup-ms", type=float, default=None,
                     help="fidelity: in-region warm-up time per sample (default 3 ms; 0: one warm-up launch)")
-    ap.add_argument("--warmup-mode", default="time", choices=("time", "clock"),
-                    help="fidelity: warm up by time, or until the probe's clock reaches its calibration median")
+    ap.add_argument("--warmup-mode", default=None, choices=("time", "clock"),
+                    help="fidelity: warm up until the probe's slowest-wave clock reaches its calibration median "
+                         "(clock, the default), or for a fixed time (time)")
     ap.add_argument("--sessions", type=int, default=1, help="fidelity: repeats of the compared modes")
+    ap.add_argument("--dump", default=None, help="fidelity: .npz path for every sample's time and clocks")
     ap.add_argument("--durations", default=None, help="fidelity: probe durations in ms, comma-separated")
     ap.add_argument("--modes", default=None,
                     help="fidelity modes, comma-separated from control,gated,ungated,frozen")
@@ -748,7 +779,7 @@ def main():
         print(json.dumps(fidelity.run(samples=args.samples, modes=modes, siblings=args.siblings,
                                       warmup_ms=args.warmup_ms, warmup=args.warmup_mode, sessions=args.sessions,
                                       durations_ms=tuple(float(x) for x in args.durations.split(","))
-                                      if args.durations else None)), flush=True)
+                                      if args.durations else None, dump=args.dump)), flush=True)
         return
     if args.kernels:
         out = run_kernels()

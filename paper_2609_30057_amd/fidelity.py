@@ -10,11 +10,17 @@ Procedure, on one GPU:
   0. settle: probe launches back to back for about 2 s, so the device's
      clock and thermal state after earlier work (a benchmark just before)
      does not drift between the native run and the later ones;
-  1. calibrate the probe's iteration count to each target duration, alone;
+  1. calibrate the probe's iteration count to each target duration, alone,
+     and record the slowest wave's clock of those launches;
   2. native: `samples` single-shot timings per duration, alone (each sample:
-     region entry, warm-up launches for about 3 ms (or exactly one with
-     warmup_ms = 0), a 512 MiB flush, one timed launch, exit; then a 5 ms
-     off-region gap);
+     region entry, warm-up, a 512 MiB flush, one timed launch, exit; then a
+     5 ms off-region gap). The warm-up launches the probe one launch at a
+     time until its slowest wave runs at the calibration clock, at most 20
+     ms (warmup="clock", the default), or for about warmup_ms (warmup="time";
+     exactly one launch with warmup_ms = 0). Every timed launch records its
+     waves' clocks: its duration is their fixed cycle count over the slowest
+     wave's clock plus a constant launch overhead, so the clock records
+     account for every sample's time;
   3. control: the same again (native repeat);
   4. gated: the same while `siblings` processes loop generate -> inject ->
      check on 512 MiB fp16 tensors (the check_stress command) off-region,
@@ -120,7 +126,8 @@ def _settle(krex, sink, seconds):
 
 def _calibrate(krex, sink, target_ms):
     """Iterations for a probe of about target_ms alone; returns (iters, median
-    ms, median wave clock in MHz of the last calibration launches)."""
+    ms, median over the last calibration launches of each launch's slowest
+    wave clock in MHz)."""
     import torch
     iters = 20000
     for _ in range(4):
@@ -130,7 +137,7 @@ def _calibrate(krex, sink, target_ms):
     ts, mhz = [], []
     for _ in range(7):
         ts.append(krex.time_loop(krex.probe_launcher(iters, sink, clk), 2, 1)[0])
-        mhz.append(float(np.nanmedian(krex.probe_clocks(clk)["mhz"])))
+        mhz.append(float(np.nanmin(krex.probe_clocks(clk)["mhz"])))
     return iters, float(np.median(ts)), float(np.median(mhz))
 
 
@@ -145,7 +152,10 @@ def clock_summary(clk):
     with np.errstate(divide="ignore", invalid="ignore"):
         mhz = np.where(rt > 0, cyc / rt * 100.0, np.nan)
     span = (a[:, :, 3].max(axis=1) - a[:, :, 2].min(axis=1)).astype(np.float64) / 1e5
-    return {"mhz_med": np.nanmedian(mhz, axis=1), "mhz_min": np.nanmin(mhz, axis=1), "span_ms": span}
+    start_skew = (a[:, :, 2].max(axis=1) - a[:, :, 2].min(axis=1)).astype(np.float64) / 1e5
+    return {"mhz_med": np.nanmedian(mhz, axis=1), "mhz_min": np.nanmin(mhz, axis=1), "span_ms": span,
+            "start_skew_ms": start_skew, "wave_ms_max": rt.max(axis=1) / 1e5,
+            "wave_cycles_med": np.median(cyc, axis=1), "wave_cycles_max": cyc.max(axis=1)}
 
 
 def _measure(krex, plan, samples, fl, sink, gap_ms, warmup_ms=0.0, warm_clock=None):
@@ -155,7 +165,9 @@ def _measure(krex, plan, samples, fl, sink, gap_ms, warmup_ms=0.0, warm_clock=No
     settle after the siblings stop); 0: one warm-up launch. warm_clock =
     (target_mhz, cap_ms): instead, warm-up launches one at a time, each
     followed by a read of its clock record, until the median wave clock
-    reaches target_mhz (at least one launch; stop after cap_ms). Every timed
+    reaches target_mhz (at least one launch; stop after cap_ms); the clock
+    that counts is the slowest wave's, since the launch lasts as long as its
+    slowest wave. Every timed
     launch records its clocks. Returns times, drains, clock summaries and
     warm-up launch counts per duration."""
     import torch
@@ -180,7 +192,7 @@ def _measure(krex, plan, samples, fl, sink, gap_ms, warmup_ms=0.0, warm_clock=No
                     while True:
                         krex.time_loop(wfn, 0, 1)          # one launch, synchronised
                         n += 1
-                        mhz = float(np.nanmedian(krex.probe_clocks(wclk)["mhz"]))
+                        mhz = float(np.nanmin(krex.probe_clocks(wclk)["mhz"]))
                         if mhz >= target or (time.perf_counter() - t0) * 1e3 >= cap_ms:
                             break
                     ts.append(krex.time_loop(fn, 0, 1, flush_buf=fl)[0])
@@ -197,19 +209,22 @@ def _measure(krex, plan, samples, fl, sink, gap_ms, warmup_ms=0.0, warm_clock=No
 
 
 def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, modes=None, warmup_ms=None,
-        settle_s=2.0, warmup="time", sessions=1, clock_cap_ms=20.0):
+        settle_s=2.0, warmup=None, sessions=1, clock_cap_ms=None, dump=None):
     """warmup: "time" (launches for about warmup_ms in each region) or
-    "clock" (launches until the probe's clock reaches the calibration
+    "clock" (launches until the slowest wave's clock reaches the calibration
     median, at most clock_cap_ms), the same procedure for every mode, the
     native run included. sessions: how many times the compared modes are
     measured in turn after the native run (P per session in P_sessions; P is
-    the first session's)."""
+    the first session's). dump: a path for an .npz of every sample's time
+    and clock figures."""
     import torch
 
     import paper_2609_30057_amd as krex
     cfg = W.SHARED
     samples = samples or cfg["samples"]
     warmup_ms = cfg["warmup_ms"] if warmup_ms is None else warmup_ms
+    warmup = cfg["warmup"] if warmup is None else warmup
+    clock_cap_ms = cfg["clock_cap_ms"] if clock_cap_ms is None else clock_cap_ms
     durations_ms = durations_ms or cfg["probe_ms"]
     siblings = cfg["siblings"] if siblings is None else siblings
     n = sibling_elems or W.CHECK_STRESS["rows"] * W.CHECK_STRESS["cols"]
@@ -332,6 +347,19 @@ def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, mode
             r = t / native
             ok = np.isfinite(f)
             corr = float(np.corrcoef(r[ok], nat_mhz / f[ok])[0, 1]) if ok.sum() > 2 and np.std(f[ok]) > 0 else None
+            ck = clocks[k][d]
+            # where the time goes, medians over the samples: the event-timed
+            # launch = (event overhead) + (first wave start .. last wave end);
+            # that span = (start skew of the waves) + (the rest, at most the
+            # longest wave)
+            cl[m + "_decomposition_us"] = {
+                "event": round(float(np.median(t)) * 1e3, 2),
+                "event_minus_span": round(float(np.median(t - ck["span_ms"])) * 1e3, 2),
+                "span": round(float(np.median(ck["span_ms"])) * 1e3, 2),
+                "start_skew": round(float(np.median(ck["start_skew_ms"])) * 1e3, 2),
+                "longest_wave": round(float(np.median(ck["wave_ms_max"])) * 1e3, 2),
+                "wave_cycles_median": int(np.median(ck["wave_cycles_med"])),
+                "wave_cycles_max": int(np.median(ck["wave_cycles_max"]))}
             cl[m] = {"MHz_p5_p50_p95": [round(float(v), 1) for v in np.nanpercentile(f, [5, 50, 95])],
                      "MHz_min_wave_p5": round(float(np.nanpercentile(clocks[k][d]["mhz_min"], 5)), 1),
                      "corr_ratio_vs_clock_deficit": None if corr is None else round(corr, 3),
@@ -339,4 +367,13 @@ def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, mode
                      "warmup_launches_p50_p95": [int(np.median(warms[k][d])),
                                                  int(np.percentile(warms[k][d], 95))]}
         result.setdefault("clock", {})[key] = cl
+    if dump:
+        arrays = {}
+        for (mode, sess), per in times.items():
+            for d, ts in per.items():
+                tag = "%s_%d_%g" % (mode, sess, d)
+                arrays["t_" + tag] = np.asarray(ts)
+                for name, v in clocks[(mode, sess)][d].items():
+                    arrays[name + "_" + tag] = np.asarray(v)
+        np.savez_compressed(dump, **arrays)
     return result

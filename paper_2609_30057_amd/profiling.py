@@ -3,6 +3,8 @@
   python -m paper_2609_30057_amd.profiling stats  --csv DIR/..._kernel_stats.csv --out FILE.md --cmd "..."
   python -m paper_2609_30057_amd.profiling traffic --fetch DIR --write DIR --out-json profiles/traffic.json
                                                  --out FILE.md --cmd "..."
+  python -m paper_2609_30057_amd.profiling select --trace DIR/..._kernel_trace.csv --out FILE.md --cmd "..."
+                                                 NAME[@GRID] ...
   python -m paper_2609_30057_amd.profiling valu-model --rates RATES.json --trace DIR/..._kernel_trace.csv
                                                  --out FILE.md --cmd "..."
 
@@ -103,6 +105,30 @@ def cmd_stats(a):
     for r in st:
         lines.append("| `%s` | %d | %.2f | %.2f | %.2f | %.2f%% |" % (
             _short(r["name"]), r["calls"], r["avg_ns"] / 1e3, r["min_ns"] / 1e3, r["max_ns"] / 1e3, r["pct"]))
+    with open(a.out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def cmd_select(a):
+    """Per-dispatch durations of selected kernels from a kernel-trace CSV:
+    each selector is NAME or NAME@GRID (a substring of the kernel name and,
+    optionally, the grid size in work-items), so one command's launches can
+    be told apart from other launches of the same kernel."""
+    rows = _rows(a.trace)
+    lines = ["# rocprofv3 kernel trace: %s" % a.title, "", "Command (from the repository root):", "",
+             "    " + a.cmd, "", "| Kernel | Grid (work-items) | Dispatches | Median (us) | Mean (us) | Min (us) | Max (us) |",
+             "|---|---|---|---|---|---|---|"]
+    for sel in a.select:
+        name, _, grid = sel.partition("@")
+        ds = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in rows
+              if name in r["Kernel_Name"] and (not grid or int(r["Grid_Size_X"]) == int(grid))]
+        if not ds:
+            lines.append("| `%s` | %s | 0 | - | - | - | - |" % (name, grid or "any"))
+            continue
+        lines.append("| `%s` | %s | %d | %.2f | %.2f | %.2f | %.2f |" % (
+            name, grid or "any", len(ds), statistics.median(ds), statistics.mean(ds), min(ds), max(ds)))
+    if a.note:
+        lines += ["", a.note]
     with open(a.out, "w") as f:
         f.write("\n".join(lines) + "\n")
 
@@ -304,6 +330,13 @@ def main():
     t.add_argument("--workload", default="gemm_large")
     t.add_argument("--algo", default="", help="JSON {kernel: algorithmic bytes per launch}")
     t.add_argument("--rdreq", default="", help="directory of the read-request-size counter pass")
+    c = sub.add_parser("select")
+    c.add_argument("--trace", required=True)
+    c.add_argument("--out", required=True)
+    c.add_argument("--cmd", required=True)
+    c.add_argument("--title", default="")
+    c.add_argument("--note", default="")
+    c.add_argument("select", nargs="+", help="NAME or NAME@GRID")
     v = sub.add_parser("valu-model")
     v.add_argument("--rates", required=True)
     v.add_argument("--trace", required=True)
@@ -316,6 +349,8 @@ def main():
         cmd_stats(a)
     elif a.cmd_name == "traffic":
         cmd_traffic(a)
+    elif a.cmd_name == "select":
+        cmd_select(a)
     else:
         cmd_valu_model(a)
 

@@ -40,12 +40,17 @@ GEMM_LARGE = dict(name="gemm_large", n=4096, dtype=BF16, dist=1, p0=0.0, p1=1.0,
                   reps=200, warmup=10, flush_bytes=GIB)
 CHECK_STRESS = dict(name="check_stress", rows=16384, cols=16384, dtype=F16, dist=0, p0=-4.0, p1=4.0, seed=2,
                     mask_seed=3, rate=0.001, delta=0.5, mode=1, rtol=1e-3, atol=1e-3)
-# warmup_ms: in-region warm-up launches of the probe for about 3 ms before
-# the flush and the timed launch (do_bench warms up by time, Section 8); a
-# single warm-up launch leaves the clocks of a device that just ran the
-# siblings' work unsettled for the 0.1 ms probe.
+# warmup: in-region warm-up of the probe before the flush and the timed
+# launch (do_bench warms up before timing, Section 8). "clock": launches one
+# at a time until the slowest wave's shader clock reaches the median the
+# probe ran at in calibration (at most clock_cap_ms). On one MI355X a probe
+# launch lasts its waves' fixed cycle count over the slowest XCD's clock plus
+# a constant 3.8 us, and a region entered right after the siblings' memory
+# load starts 1-1.4% below the clock of an idle device; the clock warm-up
+# removes that difference, where a fixed 3 ms of warm-up ("time", warmup_ms)
+# leaves it.
 SHARED = dict(name="shared", probe_ms=(0.1, 1.0, 10.0), siblings=7, samples=1000, flush_bytes=512 * MIB,
-              gap_ms=5.0, warmup_ms=3.0)
+              gap_ms=5.0, warmup="clock", warmup_ms=3.0, clock_cap_ms=20.0)
 MIXED_STREAM = dict(name="mixed_stream", commands=64, seed=4, delta=1.0, mode=0, flush_bytes=512 * MIB)
 
 
