@@ -100,19 +100,20 @@ class pinned_core:
         return False
 
 
-def cpu_baseline(step_bytes):
+def cpu_baseline(step_bytes, c_bits, cref):
     """The oracle (single-threaded C) on a bounded sample of one step: both
-    generated matrices and the full check, plus 20 of the 200 1 GiB flushes
-    (host fill of a pre-touched buffer), scaled to one step's byte mix. Runs
-    pinned to one core."""
+    generated matrices and the full check of the step's own candidate C
+    (bf16 bits) against its fp32 reference (host copies), plus 20 of the 200
+    1 GiB flushes (host fill of a pre-touched buffer), scaled to one step's
+    byte mix. Runs pinned to one core; the check's record must equal the GPU's."""
     with pinned_core() as pc:
-        out = _cpu_baseline(step_bytes)
+        out = _cpu_baseline(step_bytes, c_bits, cref)
     out.update(host_facts())
     out["core"] = pc.core
     return out
 
 
-def _cpu_baseline(step_bytes):
+def _cpu_baseline(step_bytes, c_bits, cref):
     import numpy as np
     import oracle
     from paper_2609_30057_amd import workloads as W
@@ -123,9 +124,8 @@ def _cpu_baseline(step_bytes):
     A = oracle.gen("bf16", n2, cfg["seed"], offA, 1, 0.0, 1.0)
     B = oracle.gen("bf16", n2, cfg["seed"], offB, 1, 0.0, 1.0)
     t_gen = time.perf_counter() - t0
-    cref = oracle.gen("f32", n2, 77, 0, 1, 0.0, 1.0)      # reference-shaped fp32 operand
     t0 = time.perf_counter()
-    oracle.check(A, "bf16", cref, "f32", cfg["rtol"], cfg["atol"])
+    rec = oracle.check(c_bits, "bf16", cref, "f32", cfg["rtol"], cfg["atol"])
     t_check = time.perf_counter() - t0
     buf = np.zeros(GIB // 4, dtype=np.uint32)
     oracle.flush_fill(buf, 1)                              # first touch, not timed
@@ -142,9 +142,10 @@ def _cpu_baseline(step_bytes):
         "cores": 1,
         "kind": "oracle",
         "sample": ("one gemm_large step on the host: generation of both 4096x4096 bf16 normal matrices "
-                   "(%.2f s), the full 16.8M-element bf16-vs-fp32 check against a seeded fp32 operand of "
-                   "the reference's shape (%.2f s), and 20 of the 200 1 GiB flush fills scaled x10 (%.2f s); "
+                   "(%.2f s), the full 16.8M-element check of the step's bf16 candidate C against its fp32 "
+                   "reference (%.2f s), and 20 of the 200 1 GiB flush fills scaled x10 (%.2f s); "
                    "single-threaded C oracle pinned to one core" % (t_gen, t_check, t_flush)),
+        "check_record": rec,
     }
 
 
@@ -275,7 +276,15 @@ def run_gemm_large(steps, warmup, with_cpu):
                     "argmax_abs": v.argmax_abs, "max_rel": v.max_rel},
     }
     if with_cpu:
-        out["cpu_baseline"] = cpu_baseline(step_bytes)
+        import numpy as np
+        c_bits = C.view(torch.int16).view(-1).cpu().numpy().view(np.uint16)
+        cref = Cref.view(-1).cpu().numpy()
+        out["cpu_baseline"] = cpu_baseline(step_bytes, c_bits, cref)
+        rec = out["cpu_baseline"]["check_record"]
+        gpu_rec = {"mismatches": v.mismatches, "nan_count": v.nan_count, "argmax_abs": v.argmax_abs,
+                   "max_abs": v.max_abs, "max_rel": v.max_rel}
+        out["cpu_baseline"]["check_record_equals_gpu"] = all(rec[k] == x for k, x in gpu_rec.items())
+        del out["cpu_baseline"]["check_record"]
     return out
 
 

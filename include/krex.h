@@ -34,6 +34,15 @@
  *    the work (Section 5, AMD), or at once when the launch fails (Section
  *    4.2: the counter is decremented on error returns too). Without
  *    krex_attach the kernel entry points run ungated.
+ *  - Chunking: with KREX_CHUNK_BYTES set (bytes, 0 or unset = off) a gated
+ *    process splits krex_gen, krex_gen_packed, krex_inject, krex_gen_inject
+ *    and krex_flush calls larger than that into launches of at most that
+ *    many output bytes (multiples of 64 elements), each admitted on its own,
+ *    with at most KREX_CHUNK_DEPTH (default 2) in flight: the call then
+ *    waits on the host for its oldest chunk before submitting the next. A
+ *    region entered by another process drains at most that many chunks of
+ *    the call (Section 4.2, step 3); the values written are the same.
+ *    krex_check is never split.
  *  - Failures are explicit (Section 4.3: unsupported calls fail rather than
  *    bypass): a HIP error returns KREX_EHIP and krex_last_hip_error() gives
  *    the hipError_t of the calling thread.

@@ -211,6 +211,81 @@ krex_status submit(hipStream_t s, F &&launch_fn)
     return KREX_OK;
 }
 
+// Chunked submission (KREX_CHUNK_BYTES, off when unset or 0): a gated
+// process splits a large generation, injection or flush into launches of at
+// most that many output bytes, each admitted through counter-and-gate on its
+// own, and keeps at most KREX_CHUNK_DEPTH (default 2) of them in flight,
+// waiting for the oldest before it submits the next. A region entered by
+// another process then waits for at most that many chunks of this call
+// (Section 4.2 step 3: the drain), not for the whole tensor, and the rest
+// parks at the closed gate. Generation and injection are counter-based, so
+// a chunk [j0, j0 + m) is the same call on the shifted pointers and offsets
+// and writes the same values. Chunk lengths are multiples of 64 elements,
+// which keeps aligned calls on their vector paths.
+uint64_t chunk_bytes()
+{
+    static const uint64_t v = [] {
+        const char *e = getenv("KREX_CHUNK_BYTES");
+        return e ? (uint64_t)strtoull(e, nullptr, 10) : 0ull;
+    }();
+    return v;
+}
+
+uint32_t chunk_depth()
+{
+    static const uint32_t v = [] {
+        const char *e = getenv("KREX_CHUNK_DEPTH");
+        const unsigned long d = e ? strtoul(e, nullptr, 10) : 2ul;
+        return (uint32_t)(d == 0 ? 1 : (d > 16 ? 16 : d));
+    }();
+    return v;
+}
+
+// Events marking the chunks in flight, per thread and device.
+hipEvent_t *chunk_events(int dev, uint32_t count)
+{
+    thread_local int ev_dev = -1;
+    thread_local std::vector<hipEvent_t> ev;
+    if (ev_dev != dev) {
+        ev.clear();   // events of another device stay allocated; a thread rarely switches
+        ev_dev = dev;
+    }
+    while (ev.size() < count) {
+        hipEvent_t e = nullptr;
+        if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return nullptr;
+        ev.push_back(e);
+    }
+    return ev.data();
+}
+
+// launch(j0, m) enqueues elements [j0, j0 + m) of an n-element call whose
+// elements are `elem_bytes` each.
+template <typename F>
+krex_status submit_chunked(hipStream_t s, uint64_t n, uint64_t elem_bytes, F &&launch)
+{
+    const uint64_t cb = chunk_bytes();
+    const bool chunk = cb != 0 && krexg::attached() && krexg::gated() && !krexg::intercepted() && !krexg::in_region();
+    uint64_t per = chunk ? cb / elem_bytes : n;
+    per -= per % 64;
+    if (!chunk || per == 0 || n <= per) return submit(s, [&] { return launch(0, n); });
+    const uint32_t depth = chunk_depth();
+    hipEvent_t *ev = chunk_events(current_device(), depth);
+    if (!ev) return hip_fail(hipErrorOutOfMemory);
+    uint64_t k = 0;
+    for (uint64_t j0 = 0; j0 < n; j0 += per, ++k) {
+        if (k >= depth) {
+            const hipError_t e = hipEventSynchronize(ev[k % depth]);
+            if (e != hipSuccess) return hip_fail(e);
+        }
+        const uint64_t m = (n - j0) < per ? (n - j0) : per;
+        const krex_status st = submit(s, [&] { return launch(j0, m); });
+        if (st != KREX_OK) return st;
+        const hipError_t e = hipEventRecord(ev[k % depth], s);
+        if (e != hipSuccess) return hip_fail(e);
+    }
+    return KREX_OK;
+}
+
 // Cached timing events for the timed loop, per device.
 std::mutex g_ev_mu;
 std::vector<hipEvent_t> g_timing_events[64];
@@ -335,7 +410,9 @@ krex_status krex_gen(void *dst, int32_t dtype, uint64_t n, uint64_t seed, uint64
     if (!aligned(dst, es)) return KREX_EALIGN;
     if (n == 0) return KREX_OK;
     hipStream_t s = (hipStream_t)stream;
-    return submit(s, [&] { return krex::launch_gen(dst, dtype, n, seed, offset, dist, p0, p1, s); });
+    return submit_chunked(s, n, es, [&](uint64_t j0, uint64_t m) {
+        return krex::launch_gen((uint8_t *)dst + j0 * es, dtype, m, seed, offset + j0, dist, p0, p1, s);
+    });
 }
 
 krex_status krex_gen_packed(void *dst, int32_t dtype, uint64_t n, uint64_t seed, uint64_t offset, int32_t dist,
@@ -349,7 +426,9 @@ krex_status krex_gen_packed(void *dst, int32_t dtype, uint64_t n, uint64_t seed,
     if (!aligned(dst, es)) return KREX_EALIGN;
     if (n == 0) return KREX_OK;
     hipStream_t s = (hipStream_t)stream;
-    return submit(s, [&] { return krex::launch_gen_packed(dst, dtype, n, seed, offset, dist, p0, p1, s); });
+    return submit_chunked(s, n, es, [&](uint64_t j0, uint64_t m) {
+        return krex::launch_gen_packed((uint8_t *)dst + j0 * es, dtype, m, seed, offset + j0, dist, p0, p1, s);
+    });
 }
 
 krex_status krex_transform_words(void *dst, int32_t dtype, uint64_t n, const uint32_t *words, int32_t dist, float p0,
@@ -385,7 +464,10 @@ krex_status krex_inject(void *y, const void *x, int32_t dtype, uint64_t n, uint6
     double t = floor(rate * 4294967296.0);
     const uint64_t T = t <= 0.0 ? 0ull : (t >= 4294967296.0 ? (1ull << 32) : (uint64_t)t);
     hipStream_t s = (hipStream_t)stream;
-    return submit(s, [&] { return krex::launch_inject(y, x, dtype, n, mask_seed, mask_offset, T, delta, mode, s); });
+    return submit_chunked(s, n, es, [&](uint64_t j0, uint64_t m) {
+        return krex::launch_inject((uint8_t *)y + j0 * es, (const uint8_t *)x + j0 * es, dtype, m, mask_seed,
+                                   mask_offset + j0, T, delta, mode, s);
+    });
 }
 
 krex_status krex_gen_inject(void *x, void *y, int32_t dtype, uint64_t n, uint64_t seed, uint64_t offset,
@@ -407,9 +489,9 @@ krex_status krex_gen_inject(void *x, void *y, int32_t dtype, uint64_t n, uint64_
     double t = floor(rate * 4294967296.0);
     const uint64_t T = t <= 0.0 ? 0ull : (t >= 4294967296.0 ? (1ull << 32) : (uint64_t)t);
     hipStream_t s = (hipStream_t)stream;
-    return submit(s, [&] {
-        return krex::launch_gen_inject(x, y, dtype, n, seed, offset, dist, p0, p1, mask_seed, mask_offset, T, delta,
-                                       mode, s);
+    return submit_chunked(s, n, 2 * es, [&](uint64_t j0, uint64_t m) {
+        return krex::launch_gen_inject((uint8_t *)x + j0 * es, (uint8_t *)y + j0 * es, dtype, m, seed, offset + j0,
+                                       dist, p0, p1, mask_seed, mask_offset + j0, T, delta, mode, s);
     });
 }
 
@@ -501,7 +583,9 @@ krex_status krex_flush(void *buf, uint64_t bytes, uint32_t pattern, void *stream
     if (!aligned(buf, 16)) return KREX_EALIGN;
     if (bytes == 0) return KREX_OK;
     hipStream_t s = (hipStream_t)stream;
-    return submit(s, [&] { return krex::launch_flush(buf, bytes, pattern, s); });
+    return submit_chunked(s, bytes / 16, 16, [&](uint64_t j0, uint64_t m) {
+        return krex::launch_flush((uint8_t *)buf + j0 * 16, m * 16, pattern, s);
+    });
 }
 
 krex_status krex_probe(uint64_t iters, float *sink, void *stream)

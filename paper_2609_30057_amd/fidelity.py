@@ -27,6 +27,10 @@ Procedure, on one GPU:
      every submission through counter-and-gate;
   5. ungated: the same with every process registered without gating, so
      nothing excludes the siblings from the timed interval;
+  5b. gated_chunked (optional): gated, with the siblings splitting their
+     generation and injection into separately admitted 64 MiB launches, at
+     most two in flight (KREX_CHUNK_BYTES), so a region's drain waits for
+     less sibling work;
   6. frozen (optional): gated, and the holder's regions also stop the
      siblings' process trees and pin the timing thread (CPU exclusivity,
      Section 4.2 steps 4, 5 and 7); frozen_nopin stops them without pinning;
@@ -51,7 +55,10 @@ from . import workloads as W
 MIB = 1 << 20
 
 
-def _sibling(shm, gated, n, stop, ready, q):
+def _sibling(shm, gated, n, stop, ready, q, chunk_bytes=0):
+    if chunk_bytes:
+        # read by the library at its first chunkable call in this process
+        os.environ["KREX_CHUNK_BYTES"] = str(chunk_bytes)
     import torch
 
     import paper_2609_30057_amd as krex
@@ -266,11 +273,12 @@ def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, mode
         if mode in ("torch_gated", "torch_ungated"):
             stop_path = "/tmp/krex-fid-stop-%s" % uuid.uuid4().hex[:10]
             torch_procs = _torch_siblings(siblings, shm if mode == "torch_gated" else None, stop_path)
-        if mode in ("gated", "ungated", "frozen", "frozen_nopin"):
+        if mode in ("gated", "ungated", "frozen", "frozen_nopin", "gated_chunked"):
             readies = []
+            chunk = cfg["chunk_bytes"] if mode == "gated_chunked" else 0
             for _ in range(siblings):
                 ready = ctx.Event()
-                p = ctx.Process(target=_sibling, args=(shm, gated, n, stop, ready, q))
+                p = ctx.Process(target=_sibling, args=(shm, gated, n, stop, ready, q, chunk))
                 p.start()
                 procs.append(p)
                 readies.append(ready)

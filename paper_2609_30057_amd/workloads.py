@@ -50,7 +50,7 @@ CHECK_STRESS = dict(name="check_stress", rows=16384, cols=16384, dtype=F16, dist
 # removes that difference, where a fixed 3 ms of warm-up ("time", warmup_ms)
 # leaves it.
 SHARED = dict(name="shared", probe_ms=(0.1, 1.0, 10.0), siblings=7, samples=1000, flush_bytes=512 * MIB,
-              gap_ms=5.0, warmup="clock", warmup_ms=3.0, clock_cap_ms=20.0)
+              gap_ms=5.0, warmup="clock", warmup_ms=3.0, clock_cap_ms=20.0, chunk_bytes=64 * MIB)
 MIXED_STREAM = dict(name="mixed_stream", commands=64, seed=4, delta=1.0, mode=0, flush_bytes=512 * MIB)
 
 
