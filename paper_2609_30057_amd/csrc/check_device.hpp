@@ -613,19 +613,25 @@ __device__ __forceinline__ void check_body(const uint8_t *a, const Ref &ref, uin
 
 // ------------------------------------------------------------ host helpers
 
-// Blocks of `kern` (kThreads threads) the current device holds at once,
-// capped at the partial buffer's capacity; cached per device in `cache`.
-inline uint32_t resident_blocks(const void *kern, uint32_t (&cache)[64])
+// Blocks of `kern` (kThreads threads) the current device holds at once, at
+// most per_cu_cap per compute unit (0: no cap; KREX_CHECK_BLOCKS_PER_CU
+// overrides a nonzero cap), capped at the partial buffer's capacity; cached
+// per device in `cache`.
+inline uint32_t resident_blocks(const void *kern, uint32_t (&cache)[64], uint32_t per_cu_cap = 0)
 {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = -1;
     if (dev >= 0 && cache[dev]) return cache[dev];
     int per_cu = 0, cus = 0;
     uint32_t r = kMaxCheckBlocks / 2;
+    static const uint32_t cap_env = tune_env("KREX_CHECK_BLOCKS_PER_CU", 0);
+    if (per_cu_cap && cap_env) per_cu_cap = cap_env;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kThreads, 0) == hipSuccess &&
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev < 0 ? 0 : dev) == hipSuccess &&
-        per_cu > 0 && cus > 0)
+        per_cu > 0 && cus > 0) {
+        if (per_cu_cap && (uint32_t)per_cu > per_cu_cap) per_cu = (int)per_cu_cap;
         r = (uint32_t)per_cu * (uint32_t)cus;
+    }
     if (r > (uint32_t)kMaxCheckBlocks) r = kMaxCheckBlocks;
     if (dev >= 0) cache[dev] = r;
     return r;

@@ -910,6 +910,21 @@ hipError_t launch_check_final(const CheckPartial *partials, uint32_t nblocks, ui
     return launch(k_check_final, dim3(1), dim3(kFinalThreads), s, partials, nblocks, n, out);
 }
 
+// Blocks per compute unit of the check's one resident round when both
+// operands stream from memory. Every block sweeps its own region, and on
+// gfx950 the fewer regions are read at once, the closer two streams come to
+// the read rate of a dispatch-ordered grid: 2 blocks per CU took fp16 x fp16
+// (1 GiB) from 169-170 to 164-165 us, fp32 x fp32 (512 MiB) from 86-87 to
+// 82-86 us and the 16.8M-element bf16 x fp32 check from 23.7 to 22.2 us per
+// call, against the 5-6 blocks occupancy allows (1 per CU: 218 us). Pairs
+// with an fp8 operand (16 elements per chunk) issue more per byte and keep
+// the occupancy limit (fp8 x fp8 94 us at 5 per CU, 96-102 us at 2).
+template <int DA, int DB>
+static constexpr uint32_t check_blocks_per_cu()
+{
+    return chunk_elems<DA, DB>() == 16 ? 0u : 2u;
+}
+
 template <int DA, int DB, int D>
 static hipError_t check_ab_d(const void *a, const void *b, uint64_t n, float rtol, float atol, void *scratch,
                              krex_check_result *out, hipStream_t s)
@@ -917,7 +932,8 @@ static hipError_t check_ab_d(const void *a, const void *b, uint64_t n, float rto
     constexpr int E = chunk_elems<DA, DB>();
     const bool vec = (((uintptr_t)a & 15u) == 0 && ((uintptr_t)b & 15u) == 0);
     static uint32_t cache_vec[64] = {}, cache_el[64] = {};
-    const uint64_t resident = vec ? resident_blocks((const void *)k_check<DA, DB, true, D>, cache_vec)
+    const uint64_t resident = vec ? resident_blocks((const void *)k_check<DA, DB, true, D>, cache_vec,
+                                                    check_blocks_per_cu<DA, DB>())
                                   : resident_blocks((const void *)k_check<DA, DB, false, 2>, cache_el);
     uint32_t U, G;
     check_grid(n / E, resident, &U, &G);
