@@ -103,12 +103,15 @@ static constexpr float kMinPositive = 0x1p-149f;
 // pair). NOINF: neither operand type has an infinity and their difference
 // cannot overflow (fp8 e4m3fn pairs: |a|, |b| <= 448), so |a - b| is already
 // 0 for equal operands and the threshold is finite: no select, no clamp; and
-// the candidate test is fl(d Rup) > |b| with Rup >= (1/R)(1 + 2^-21) (see
-// RatioFilter), one product and one compare. Mismatches are counted here;
-// unordered pairs are counted by the caller.
+// the candidate test is d Rup > |b| with Rup >= (1/R)(1 + 2^-21) (see
+// RatioFilter), decided exactly by the sign of fma(d, Rup, -|b|): the lane's
+// largest such residual over a chunk goes to tmax (the non-propagating
+// maximum, so an unordered pair, NaN there, hides no other element) and the
+// caller takes one ballot of tmax > 0 per chunk instead of one per element.
+// Mismatches are counted here; unordered pairs are counted by the caller.
 template <bool NOINF>
 __device__ __forceinline__ float elem_verdict(float A, float B, float rtol, float atol, float R, float Rup,
-                                              LaneAcc &acc, uint64_t &cand)
+                                              LaneAcc &acc, uint64_t &cand, float &tmax)
 {
     const float d0 = __builtin_fabsf(A - B);
     const float ab = __builtin_fabsf(B);
@@ -116,7 +119,7 @@ __device__ __forceinline__ float elem_verdict(float A, float B, float rtol, floa
     const float rt = rtol * ab;
     const float thr = NOINF ? atol + rt : __builtin_fminf(atol + rt, 0x1.fffffep127f);
     acc.mism += (d <= thr) ? 0u : 1u;
-    if constexpr (NOINF) cand |= __ballot(d * Rup > ab);
+    if constexpr (NOINF) tmax = __builtin_fmaxf(tmax, __builtin_fmaf(d, Rup, -ab));
     else cand |= __ballot(d >= __builtin_fmaxf(R * ab, kMinPositive));
     return d;
 }
@@ -127,7 +130,8 @@ template <bool NOINF>
 __device__ __forceinline__ float check_elem(float A, float B, float rtol, float atol, LaneAcc &acc)
 {
     uint64_t cand = 0;
-    const float d = elem_verdict<NOINF>(A, B, rtol, atol, kRatioFloor, 0.0f, acc, cand);
+    float tmax = 0.0f;
+    const float d = elem_verdict<NOINF>(A, B, rtol, atol, kRatioFloor, 0.0f, acc, cand, tmax);
     acc.wnan += popc(__ballot(__builtin_isunordered(A, B)));
     ratio_update(A, B, acc);
     return d;
@@ -387,10 +391,12 @@ template <int E>
 struct RatioFilter {
     float R = kRatioFloor;
     // An upper bound of 1/R, at least (1/R)(1 + 2^-21): fl(1/R) (correctly
-    // rounded) times 1 + 2^-20. For fp8 pairs (|b| is 0 or at least 2^-9, d
-    // at most 896) an element with ratio d/|b| > R has d Rup > |b|(1 + 2^-21),
-    // at least four units in the last place of |b| above it (or above 0), so
-    // fl(d Rup) > |b|; an element with fl(d Rup) <= |b| therefore has ratio
+    // rounded) times 1 + 2^-20. For fp8 pairs an element with ratio
+    // d/|b| > R has d Rup > |b| exactly, so fma(d, Rup, -|b|), the rounded
+    // exact residual, is positive (no underflow to zero: d and |b| are
+    // multiples of 2^-9 and Rup, at least 2^-20 when finite R <= 896 2^9, a
+    // multiple of 2^-43, so a nonzero residual is at least 2^-52); an
+    // element whose residual is not positive has ratio
     // <= R, below the maximum, and is skipped. R = +inf gives Rup = 0.
     float Rup = 0x1.00001p32f;
 
@@ -455,12 +461,14 @@ __device__ __forceinline__ void check_body(const uint8_t *a, const Ref &ref, uin
     // unordered pairs and take the maximum again without them.
     auto process = [&](const float (&A)[E], const float (&B)[E], uint64_t c) -> uint64_t {
         float cmax = -1.0f;
+        float tmax = 0.0f;
         uint64_t cand = 0;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-            const float d = elem_verdict<NOINF>(A[e], B[e], rtol, atol, rf.R, rf.Rup, acc, cand);
+            const float d = elem_verdict<NOINF>(A[e], B[e], rtol, atol, rf.R, rf.Rup, acc, cand, tmax);
             cmax = __builtin_elementwise_maximum(cmax, d);
         }
+        if constexpr (NOINF) cand = __ballot(tmax > 0.0f);
         // the counts are complete here: kept from being moved past the rare
         // branch below, where their operands would need extra registers
         __asm__ volatile("" : "+v"(acc.mism));
