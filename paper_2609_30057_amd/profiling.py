@@ -7,6 +7,8 @@
                                                  NAME[@GRID] ...
   python -m paper_2609_30057_amd.profiling valu-model --rates RATES.json --trace DIR/..._kernel_trace.csv
                                                  --out FILE.md --cmd "..."
+  python -m paper_2609_30057_amd.profiling throughput --csv DIR/..._kernel_stats.csv --out FILE.md --cmd "..."
+  python -m paper_2609_30057_amd.profiling sq --dir DIR --out FILE.md --cmd "..."
 
 valu-model: for the one-unit-per-thread kernels (generation), the vector
 instructions of the per-unit path in the gfx950 assembly (from the loop head
@@ -173,6 +175,155 @@ def default_algo(workload):
             "krex::k_flush": cfg["flush_bytes"]}
 
 
+# The launches of bench.py --kernels: what each one is and what bounds it.
+KERNEL_ROWS = [
+    ("generation, fp32 uniform, 67M", "krex::k_gen<0, 0, true>", "HBM write"),
+    ("generation, fp16 uniform, 268M", "krex::k_gen<2, 0, true>", "issue + HBM (Philox word per element)"),
+    ("generation, bf16 normal, 16.8M (bench)", "krex::k_gen<1, 1, false>", "vector issue"),
+    ("generation, fp32 normal, 16.8M", "krex::k_gen<0, 1, false>", "vector issue"),
+    ("generation, fp8 normal, 268M", "krex::k_gen<3, 1, false>", "vector issue"),
+    ("packed generation, fp16 uniform, 268M", "krex::k_gen_packed<2, 0, 2>", "HBM write"),
+    ("packed generation, bf16 normal, 16.8M", "krex::k_gen_packed<1, 1, 0>", "vector issue"),
+    ("packed generation, fp8 uniform, 268M", "krex::k_gen_packed<3, 0, 2>", "HBM write / issue"),
+    ("packed generation, fp8 normal, 268M", "krex::k_gen_packed<3, 1, 0>", "vector issue"),
+    ("injection, fp16 exact, 268M", "krex::k_inject<2, 1>", "HBM read + write"),
+    ("generation + injection in one launch, fp16 uniform exact, 268M", "krex::k_gen_inject<2, 0, true, 1>",
+     "vector issue (value + mask word per element)"),
+    ("check, bf16 x fp32, 16.8M (bench)", "krex::k_check<1, 0, true, 2>", "HBM read (small launch)"),
+    ("check, fp16 x fp16, 268M", "krex::k_check<2, 2, true, 3>", "HBM read"),
+    ("check, fp8 x fp8, 268M", "krex::k_check<3, 3, true, 3>", "HBM read (latency: half the time issuing)"),
+    ("check, fp32 x fp32, 67M", "krex::k_check<0, 0, true, 2>", "HBM read"),
+    ("check vs regenerated reference, fp32 x fp32 uniform, 67M", "krex::k_check_gen<0, 0, 0, true, true, 2>",
+     "issue + HBM read (candidate only)"),
+    ("check vs regenerated reference, bf16 x fp32 normal, 16.8M", "krex::k_check_gen<1, 0, 1, false, true, 2>",
+     "vector issue (normal transform)"),
+    ("check vs regenerated reference, fp16 x fp16 uniform, 268M", "krex::k_check_gen<2, 2, 0, true, true, 2>",
+     "vector issue (a Philox word per element)"),
+    ("check vs regenerated reference, fp8 x fp8 normal, 268M", "krex::k_check_gen<3, 3, 1, false, true, 2>",
+     "vector issue (normal transform)"),
+    ("check vs regenerated packed reference, fp16 x fp16 uniform, 268M",
+     "krex::k_check_gen_packed<2, 2, 0, 2, true, 2>", "vector issue (a Philox block per 8 elements)"),
+    ("check vs regenerated packed reference, fp8 x fp8 uniform, 268M",
+     "krex::k_check_gen_packed<3, 3, 0, 2, true, 2>", "vector issue (a Philox block per 16 elements)"),
+    ("flush, 1 GiB", "krex::k_flush", "HBM write"),
+]
+
+HBM_PEAK = 8.0e12
+
+
+def _own_command():
+    """This summarizer's invocation, without its free-text arguments."""
+    import sys
+    out, skip = [], False
+    for x in sys.argv[1:]:
+        if skip:
+            skip = False
+            continue
+        if x in ("--cmd", "--note", "--tail", "--title"):
+            skip = True
+            continue
+        out.append(x)
+    return "python3 -m paper_2609_30057_amd.profiling " + " ".join(out)
+
+
+def cmd_throughput(a):
+    """Per-kernel throughput of bench.py --kernels from its kernel-trace
+    statistics: algorithmic bytes per launch over the average duration."""
+    st = {_short(r["name"]): r for r in kernel_stats(a.csv)}
+    algo = kernels_algo()
+    lines = ["# Per-kernel throughput on the commands' shapes, one MI355X", "",
+             "Commands (from the repository root):", "", "    " + a.cmd.replace(" ;; ", "\n    "),
+             "    " + _own_command(), ""]
+    if a.note:
+        lines += [a.note, ""]
+    lines += ["| Kernel and shape | Kernel | Time (us) | GB/s | Fraction of 8 TB/s | Bound |",
+              "|---|---|---|---|---|---|"]
+    for label, k, bound in KERNEL_ROWS:
+        r = st.get(k)
+        if r is None:
+            lines.append("| %s | `%s` | - | - | - | %s |" % (label, k, bound))
+            continue
+        t = r["avg_ns"] * 1e-9
+        bw = algo[k] / t
+        lines.append("| %s | `%s` | %.1f | %.0f | %.3f | %s |" % (label, k, t * 1e6, bw / 1e9, bw / HBM_PEAK, bound))
+    fin = st.get("krex::k_check_final")
+    if fin:
+        lines += ["", "`krex::k_check_final` (the check's second launch): %d calls, average %.2f us." % (
+            fin["calls"], fin["avg_ns"] / 1e3)]
+    if a.tail:
+        lines += ["", a.tail]
+    with open(a.out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+_DT_SIZE = {0: 4, 1: 2, 2: 2, 3: 1, 4: 4}
+
+
+def _units(name, algo_bytes):
+    """16-byte units of a --kernels launch: one vector of output
+    (generation, injection, flush) or of the narrower operand (checks)."""
+    m = re.search(r"<(.*)>", name)
+    args = [int(x) if x.isdigit() else x for x in (m.group(1).split(", ") if m else [])]
+    if "k_check_gen" in name:
+        sa, sb = _DT_SIZE[args[0]], _DT_SIZE[args[1]]
+        return algo_bytes / sa * min(sa, sb) / 16
+    if "k_check<" in name:
+        sa, sb = _DT_SIZE[args[0]], _DT_SIZE[args[1]]
+        return algo_bytes / (sa + sb) * min(sa, sb) / 16
+    if "k_inject" in name or "k_gen_inject" in name:
+        return algo_bytes / 32
+    return algo_bytes / 16
+
+
+def cmd_sq(a):
+    """SQ counters per kernel from a --pmc run with --kernel-trace (medians
+    over each kernel's dispatches at its largest grid)."""
+    files = glob.glob(os.path.join(a.dir, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit("no counter_collection.csv under %s" % a.dir)
+    disp = {}
+    for fpath in files:
+        for r in _rows(fpath):
+            key = (fpath, r["Dispatch_Id"])
+            d = disp.setdefault(key, {"name": _short(r["Kernel_Name"]), "grid": int(r["Grid_Size"]),
+                                      "ns": int(r["End_Timestamp"]) - int(r["Start_Timestamp"])})
+            d[r["Counter_Name"]] = float(r["Counter_Value"])
+    per = {}
+    for d in disp.values():
+        per.setdefault(d["name"], []).append(d)
+    algo = kernels_algo()
+    lines = ["# SQ counters per kernel (gfx950, one MI355X)", "", "Commands (from the repository root):", "",
+             "    " + a.cmd.replace(" ;; ", "\n    "), "    " + _own_command(), ""]
+    if a.note:
+        lines += [a.note, ""]
+    lines += ["| Kernel | us | waves | VALU / wave | SALU / wave | VALU per lane-unit | clock (MHz) | waves/SIMD "
+              "| issue-waiting/SIMD |", "|---|---|---|---|---|---|---|---|---|"]
+    order = [k for _, k, _ in KERNEL_ROWS] + sorted(k for k in per if k not in [r[1] for r in KERNEL_ROWS])
+    med = statistics.median
+    for k in order:
+        if k not in per:
+            continue
+        g = max(d["grid"] for d in per[k])
+        ds = [d for d in per[k] if d["grid"] == g]
+        us = med([d["ns"] for d in ds]) / 1e3
+        waves = med([d.get("SQ_WAVES", 0.0) for d in ds])
+        valu = med([d.get("SQ_INSTS_VALU", 0.0) for d in ds])
+        salu = med([d.get("SQ_INSTS_SALU", 0.0) for d in ds])
+        cyc = med([d.get("GRBM_GUI_ACTIVE", 0.0) for d in ds]) / a.xcds
+        wc = med([d.get("SQ_WAVE_CYCLES", 0.0) for d in ds])
+        wait = med([d.get("SQ_WAIT_INST_ANY", 0.0) for d in ds])
+        simds = 4 * a.cus
+        per_unit = "%.0f" % (valu * 64 / _units(k, algo[k])) if k in algo else "-"
+        lines.append("| `%s` | %.1f | %d | %.0f | %.0f | %s | %.0f | %.1f | %.1f |" % (
+            k.replace("krex::", ""), us, waves, valu / max(waves, 1), salu / max(waves, 1), per_unit,
+            cyc / (us * 1e-6) / 1e6 if us else 0.0, wc * 4 / (simds * cyc) if cyc else 0.0,
+            wait * 4 / (simds * cyc) if cyc else 0.0))
+    if a.tail:
+        lines += ["", a.tail]
+    with open(a.out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 def cmd_traffic(a):
     fetch = counters(a.fetch, "FETCH_SIZE")
     write = counters(a.write, "WRITE_SIZE")
@@ -337,6 +488,20 @@ def main():
     c.add_argument("--title", default="")
     c.add_argument("--note", default="")
     c.add_argument("select", nargs="+", help="NAME or NAME@GRID")
+    h = sub.add_parser("throughput")
+    h.add_argument("--csv", required=True)
+    h.add_argument("--out", required=True)
+    h.add_argument("--cmd", required=True)
+    h.add_argument("--note", default="")
+    h.add_argument("--tail", default="")
+    q = sub.add_parser("sq")
+    q.add_argument("--dir", required=True)
+    q.add_argument("--out", required=True)
+    q.add_argument("--cmd", required=True)
+    q.add_argument("--note", default="")
+    q.add_argument("--tail", default="")
+    q.add_argument("--cus", type=int, default=256)
+    q.add_argument("--xcds", type=int, default=8)
     v = sub.add_parser("valu-model")
     v.add_argument("--rates", required=True)
     v.add_argument("--trace", required=True)
@@ -351,6 +516,10 @@ def main():
         cmd_traffic(a)
     elif a.cmd_name == "select":
         cmd_select(a)
+    elif a.cmd_name == "throughput":
+        cmd_throughput(a)
+    elif a.cmd_name == "sq":
+        cmd_sq(a)
     else:
         cmd_valu_model(a)
 

@@ -145,3 +145,62 @@ def test_issue_model_of_a_generation_launch(tmp_path, asm):
     assert float(row[5]) == pytest.approx(waves * cyc / (1024 * 2.4e9) * 1e6, abs=0.06)
     assert float(row[6]) == pytest.approx((1 << 24) * 16 / 8e12 * 1e6, abs=0.06)   # HBM time of 16 B per unit
     assert float(row[8]) == pytest.approx(40.0)
+
+
+def test_throughput_table_from_kernel_stats(tmp_path):
+    """Algorithmic bytes over the average duration, for the listed launches
+    of bench.py --kernels; the check's final reduction is reported apart."""
+    path = tmp_path / "stats.csv"
+    rows = [("void krex::k_check<2, 2, true, 3>(unsigned char const*)", 23, 160000.0),
+            ("krex::k_flush(HIP_vector_type<unsigned int, 4u>*, unsigned long, unsigned int)", 23, 134217.728),
+            ("krex::k_check_final(krex::CheckPartial const*)", 46, 4000.0)]
+    with open(path, "w", newline="") as f:
+        w = csv.writer(f)
+        w.writerow(["Name", "Calls", "TotalDurationNs", "AverageNs", "Percentage", "MinNs", "MaxNs", "StdDev"])
+        for name, calls, avg in rows:
+            w.writerow([name, calls, calls * avg, avg, 1.0, avg, avg, 0.0])
+    out = tmp_path / "t.md"
+    P.cmd_throughput(Args(csv=str(path), out=str(out), cmd="rocprofv3 x", note="", tail=""))
+    text = out.read_text()
+    # 1 GiB of fp16 x fp16 operands (2^28 elements, 4 bytes each) in 160 us
+    assert "| check, fp16 x fp16, 268M | `krex::k_check<2, 2, true, 3>` | 160.0 | 6711 | 0.839 | HBM read |" in text
+    assert "| flush, 1 GiB | `krex::k_flush` | 134.2 | 8000 | 1.000 | HBM write |" in text
+    assert "| generation, fp32 uniform, 67M | `krex::k_gen<0, 0, true>` | - |" in text
+    assert "46 calls, average 4.00 us" in text
+
+
+def test_units_per_launch():
+    """16-byte units: of the output for generation and injection, of the
+    narrower operand for the checks."""
+    algo = P.kernels_algo()
+    assert P._units("krex::k_gen<2, 0, true>", algo["krex::k_gen<2, 0, true>"]) == 2**25
+    assert P._units("krex::k_inject<2, 1>", algo["krex::k_inject<2, 1>"]) == 2**25
+    assert P._units("krex::k_check<1, 0, true, 2>", algo["krex::k_check<1, 0, true, 2>"]) == 2**24 * 2 / 16
+    assert P._units("krex::k_check<3, 3, true, 3>", algo["krex::k_check<3, 3, true, 3>"]) == 2**28 / 16
+    assert P._units("krex::k_check_gen<1, 0, 1, false, true, 2>",
+                    algo["krex::k_check_gen<1, 0, 1, false, true, 2>"]) == 2**24 * 2 / 16
+
+
+def test_sq_table_from_counters(tmp_path):
+    """Per-wave instruction counts, clock, resident and issue-waiting waves
+    from one dispatch's SQ counters (8 XCDs, 256 CUs)."""
+    d = tmp_path / "sq"
+    d.mkdir()
+    k = "void krex::k_check<3, 3, true, 3>(unsigned char const*)"
+    us = 100.0
+    cyc = 2.4e9 * us * 1e-6                       # 240,000 cycles per XCD
+    vals = {"SQ_WAVES": 4096, "SQ_INSTS_VALU": 4096 * 500.0, "SQ_INSTS_SALU": 4096 * 50.0,
+            "GRBM_GUI_ACTIVE": 8 * cyc, "SQ_WAVE_CYCLES": 3.0 * 1024 * cyc / 4, "SQ_WAIT_INST_ANY": 1024 * cyc / 4}
+    with open(d / "sq_counter_collection.csv", "w", newline="") as f:
+        w = csv.DictWriter(f, FIELDS)
+        w.writeheader()
+        for c, v in vals.items():
+            w.writerow({"Correlation_Id": 1, "Dispatch_Id": 1, "Agent_Id": "Agent 1", "Queue_Id": 1,
+                        "Process_Id": 1, "Thread_Id": 1, "Grid_Size": 4096 * 64, "Kernel_Id": 1, "Kernel_Name": k,
+                        "Workgroup_Size": 256, "LDS_Block_Size": 0, "Scratch_Size": 0, "VGPR_Count": 8,
+                        "Accum_VGPR_Count": 0, "SGPR_Count": 16, "Counter_Name": c, "Counter_Value": v,
+                        "Start_Timestamp": 0, "End_Timestamp": int(us * 1000)})
+    out = tmp_path / "sq.md"
+    P.cmd_sq(Args(dir=str(d), out=str(out), cmd="rocprofv3 x", note="", tail="", cus=256, xcds=8))
+    # 2^28 fp8 pairs = 2^24 units; 4096 waves x 500 x 64 / 2^24 = 7.8 per unit
+    assert "| `k_check<3, 3, true, 3>` | 100.0 | 4096 | 500 | 50 | 8 | 2400 | 3.0 | 1.0 |" in out.read_text()
