@@ -2,8 +2,8 @@
 gates a sibling that never calls this library: a torch process looping fp32
 GEMMs. Every one of its gated batches runs between its admission and its
 completion, and none of those intervals overlaps a critical region of the
-holder (Section 5: the AMD interposer counts each queue's launches and
-releases them when their completion signal fires; Section 4.2, steps 2-3).
+holder (Section 5, the AMD variant: each admitted batch is counted until a
+barrier packet behind it completes; Section 4.2, steps 2-3).
 A process with the library loaded but no segment named passes everything
 through."""
 import json
