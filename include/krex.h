@@ -9,8 +9,8 @@
  * checks the candidate against a reference and then times it (Section 1;
  * Section 2.1). Generation and checking produce values, not timings, and
  * must give the same tensors and verdict under contention (Section 2.1,
- * "Benchmarking command"). Only the timed loop needs the device to itself;
- * it is marked as a critical region (Section 3, R1; Section 4.1), entered by
+ * "Benchmarking command"). Exclusive use of the device matters for the
+ * timed loop alone, which is marked as a critical region (Section 3, R1; Section 4.1), entered by
  * lock -> gate -> drain -> cache flush and left by wait -> reopen -> unlock
  * (Section 4.2, steps 1-3, 5, 6, 8), with the AMD variant's completion
  * counters (Section 5).
