@@ -77,8 +77,7 @@ __global__ __launch_bounds__(kThreads) void k_gen(GenParams P)
             for (int l = 0; l < 4; ++l) pk.w[l] = w.v[l];
         } else {
             words4 wb[G];
-#pragma unroll
-            for (int i = 0; i < G; ++i) wb[i] = philox_block(bfirst + i, P.rk);
+            philox_blocks<G>(bfirst, P.rk, wb);
             float v[4 * G];
 #pragma unroll
             for (int i = 0; i < G; ++i) transform4<DIST, POW2>(wb[i], P.p0, POW2 ? P.c : P.p1, v + 4 * i);

@@ -81,6 +81,56 @@ __device__ __forceinline__ words4 philox_block(uint64_t b, const RoundKeys &rk)
     return o;
 }
 
+// G consecutive blocks b, b + 1, ... in lockstep, the same values as G
+// philox_block calls. On gfx950 an instruction that reads a v_mad_u64_u32
+// result right after it issues later than an independent one, and the
+// compiler's schedule places each three-way xor next to its product. Here
+// each round forms all 2 G products, then (behind a scheduling fence, so the
+// two phases stay apart) all 2 G xors. In a plain two-block round chain this
+// took 10% fewer cycles per block than the compiler's interleaving; in the
+// kernels it took fp8 normal generation 8% and packed fp8 normal 5% faster,
+// left the uniform generators and the packed stream's check (its two-block
+// fp8 normal units included) unchanged, and made the check against a
+// regenerated word-stream reference 3% slower (the fence also holds back
+// the check's own work), which therefore keeps separate philox_block calls.
+template <int G>
+__device__ __forceinline__ void philox_blocks(uint64_t b, const RoundKeys &rk, words4 (&o)[G])
+{
+    uint32_t x0[G], x1[G], x2[G], x3[G];
+#pragma unroll
+    for (int i = 0; i < G; ++i) {
+        x0[i] = (uint32_t)(b + (uint64_t)i);
+        x1[i] = (uint32_t)((b + (uint64_t)i) >> 32);
+        x2[i] = 0u;
+        x3[i] = 0u;
+    }
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        uint64_t p0[G], p1[G];
+#pragma unroll
+        for (int i = 0; i < G; ++i) {
+            p0[i] = (uint64_t)0xD2511F53u * (uint64_t)x0[i];
+            p1[i] = (uint64_t)0xCD9E8D57u * (uint64_t)x2[i];
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < G; ++i) {
+            x0[i] = __builtin_amdgcn_bitop3_b32((uint32_t)(p1[i] >> 32), x1[i], rk.k[2 * r], 0x96);
+            x1[i] = (uint32_t)p1[i];
+            x2[i] = __builtin_amdgcn_bitop3_b32((uint32_t)(p0[i] >> 32), x3[i], rk.k[2 * r + 1], 0x96);
+            x3[i] = (uint32_t)p0[i];
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int i = 0; i < G; ++i) {
+        o[i].v[0] = x0[i];
+        o[i].v[1] = x1[i];
+        o[i].v[2] = x2[i];
+        o[i].v[3] = x3[i];
+    }
+}
+
 // ------------------------------------------------------- streaming memory
 
 // 16-byte load of a streamed operand, non-temporal: it does not allocate in
@@ -434,11 +484,13 @@ __device__ __forceinline__ void packed_unit(uint64_t unit, const RoundKeys &rk, 
     constexpr int GB = packed_of<DT, DIST>::GB;
     constexpr uint32_t kMask = (1u << W) - 1u;
     uint32_t wv[4 * GB];
+    words4 blk[GB];
+    if constexpr (GB > 1) philox_blocks<GB>(unit * GB, rk, blk);
+    else blk[0] = philox_block(unit, rk);
 #pragma unroll
     for (int i = 0; i < GB; ++i) {
-        const words4 blk = philox_block(unit * GB + i, rk);
 #pragma unroll
-        for (int l = 0; l < 4; ++l) wv[4 * i + l] = blk.v[l];
+        for (int l = 0; l < 4; ++l) wv[4 * i + l] = blk[i].v[l];
     }
     if constexpr (DIST == BITCAST) {
         static_assert(GB == 1, "bitcast units are one block");
