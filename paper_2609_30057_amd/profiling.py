@@ -416,6 +416,23 @@ def _op_cost(op, rates):
     return 4.0   # unmeasured: the half-rate cost most conversions and 64-bit operations have
 
 
+PHILOX_PAIR = "philox4x32_10 block (philox_block, two per group)"
+PHILOX_LOCKSTEP = "philox4x32_10 block (philox_blocks<2>)"
+
+
+def philox_mad_cost(rates, name):
+    """Issue cost of a v_mad_u64_u32 inside the Philox rounds of kernel
+    `name`: its measured block cost less the block's 20 three-way xors, over
+    its 20 products (the lockstep form for the word-stream generators and the
+    two-block packed units, the compiler's interleaving elsewhere); None
+    without the block entries."""
+    lock = name.startswith("krex::k_gen<") or name.startswith("krex::k_gen_packed<3, 1")
+    key = PHILOX_LOCKSTEP if lock else PHILOX_PAIR
+    if key not in rates:
+        return None
+    return (rates[key] - 20 * _op_cost("v_bitop3_b32", rates)) / 20
+
+
 def cmd_valu_model(a):
     from paper_2609_30057_amd import build as B
     rates = json.load(open(a.rates))["cycles"]
@@ -440,8 +457,14 @@ def cmd_valu_model(a):
              "cycles / (4 SIMDs x %d CUs x 2.4 GHz) at full vector issue." % a.cus, "",
              "Each unit also writes one 16-byte vector: u x 16 bytes at 8 TB/s is the launch's HBM time. The "
              "larger of the two times bounds the kernel.", "",
+             "The rate table prices `v_mad_u64_u32` on its own; inside the Philox rounds each product is read by "
+             "the next three-way xor, and the measured Philox block entries put its cost at %s cycles (lockstep "
+             "form) and %s cycles (the compiler's interleaving). The last two columns price it so." % (
+                 "%.2f" % philox_mad_cost(rates, "krex::k_gen<") if PHILOX_LOCKSTEP in rates else "-",
+                 "%.2f" % philox_mad_cost(rates, "x") if PHILOX_PAIR in rates else "-"), "",
              "| Kernel | Vector instr. per unit | Weighted cycles per unit-wave | Unit-waves | Time at full issue (us) "
-             "| HBM time (us) | Bound | Measured (us) | Fraction of the bound |", "|---|---|---|---|---|---|---|---|---|"]
+             "| HBM time (us) | Bound | Measured (us) | Fraction of the bound | Time at full issue, Philox in "
+             "context (us) | Fraction of that bound |", "|---|---|---|---|---|---|---|---|---|---|---|"]
     for name in sorted(launches):
         args = re.match(r"krex::k_gen(?:_packed)?<(.*)>", name).group(1).split(", ")
         if "packed" in name:
@@ -450,6 +473,11 @@ def cmd_valu_model(a):
             sym = "_ZN4krex5k_genILi%sELi%sELb%dEEEvNS_9GenParamsE" % (args[0], args[1], args[2] == "true")
         ops = _unit_path(asm, sym)
         cyc = sum(_op_cost(o, rates) for o in ops)
+        mad = philox_mad_cost(rates, name)
+        cyc_ctx = None
+        if mad is not None:
+            ctx = dict(rates, v_mad_u64_u32=mad)
+            cyc_ctx = sum(_op_cost(o, ctx) for o in ops)
         grid, _ = max(launches[name])
         durs = [d for g, d in launches[name] if g == grid]
         meas = statistics.median(durs)
@@ -457,8 +485,10 @@ def cmd_valu_model(a):
         waves = units / 64.0
         t = waves * cyc / (4 * a.cus * clock) * 1e6
         th = units * 16 / 8e12 * 1e6
-        lines.append("| `%s` | %d | %.0f | %d | %.1f | %.1f | %s | %.1f | %.2f |" % (
-            name, len(ops), cyc, waves, t, th, "issue" if t >= th else "HBM", meas, max(t, th) / meas))
+        tc = waves * cyc_ctx / (4 * a.cus * clock) * 1e6 if cyc_ctx is not None else None
+        lines.append("| `%s` | %d | %.0f | %d | %.1f | %.1f | %s | %.1f | %.2f | %s | %s |" % (
+            name, len(ops), cyc, waves, t, th, "issue" if t >= th else "HBM", meas, max(t, th) / meas,
+            "%.1f" % tc if tc is not None else "-", "%.2f" % (max(tc, th) / meas) if tc is not None else "-"))
     with open(a.out, "w") as f:
         f.write("\n".join(lines) + "\n")
 

@@ -204,3 +204,36 @@ def test_sq_table_from_counters(tmp_path):
     P.cmd_sq(Args(dir=str(d), out=str(out), cmd="rocprofv3 x", note="", tail="", cus=256, xcds=8))
     # 2^28 fp8 pairs = 2^24 units; 4096 waves x 500 x 64 / 2^24 = 7.8 per unit
     assert "| `k_check<3, 3, true, 3>` | 100.0 | 4096 | 500 | 50 | 8 | 2400 | 3.0 | 1.0 |" in out.read_text()
+
+
+def test_issue_model_prices_philox_products_in_context(tmp_path, asm):
+    """With the Philox block entries, a word-stream generator's products are
+    priced at (lockstep block cost - 20 three-way xors) / 20 in the last two
+    columns; without them those columns stay empty."""
+    ops = P._unit_path(asm, "_ZN4krex5k_genILi0ELi0ELb1EEEvNS_9GenParamsE")
+    cycles = dict(RATES)
+    cycles[P.PHILOX_LOCKSTEP] = 20 * 1.9 + 20 * 7.0          # a product costs 7 cycles in context
+    cycles[P.PHILOX_PAIR] = 20 * 1.9 + 20 * 8.0
+    assert P.philox_mad_cost(cycles, "krex::k_gen<0, 0, true>") == pytest.approx(7.0)
+    assert P.philox_mad_cost(cycles, "krex::k_gen_packed<2, 0, 2>") == pytest.approx(8.0)
+    assert P.philox_mad_cost(cycles, "krex::k_gen_packed<3, 1, 0>") == pytest.approx(7.0)
+    assert P.philox_mad_cost(RATES, "krex::k_gen<0, 0, true>") is None
+    trace = tmp_path / "trace.csv"
+    fields = ["Kind", "Kernel_Name", "Start_Timestamp", "End_Timestamp", "Grid_Size_X"]
+    with open(trace, "w", newline="") as f:
+        w = csv.DictWriter(f, fields)
+        w.writeheader()
+        w.writerow({"Kind": "KERNEL_DISPATCH", "Kernel_Name": "void krex::k_gen<0, 0, true>(krex::GenParams)",
+                    "Start_Timestamp": 1000, "End_Timestamp": 41000, "Grid_Size_X": 1 << 24})
+    for rates, filled in ((cycles, True), (RATES, False)):
+        rj = tmp_path / "rates.json"
+        rj.write_text(json.dumps({"cycles": rates}))
+        out = tmp_path / "m.md"
+        P.cmd_valu_model(Args(rates=str(rj), trace=str(trace), out=str(out), cmd="x", title="t", cus=256))
+        row = [l for l in out.read_text().splitlines() if "k_gen<0, 0, true>" in l][0].split("|")
+        if filled:
+            ctx = dict(rates, v_mad_u64_u32=7.0)
+            cyc = sum(P._op_cost(o, ctx) for o in ops)
+            assert float(row[10]) == pytest.approx((1 << 24) / 64 * cyc / (1024 * 2.4e9) * 1e6, abs=0.06)
+        else:
+            assert row[10].strip() == "-" and row[11].strip() == "-"
