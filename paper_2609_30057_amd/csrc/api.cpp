@@ -241,15 +241,13 @@ uint32_t chunk_depth()
     return v;
 }
 
-// Events marking the chunks in flight, per thread and device.
+// Events marking the chunks in flight, per thread and device (created with
+// that device current, kept for the thread's life).
 hipEvent_t *chunk_events(int dev, uint32_t count)
 {
-    thread_local int ev_dev = -1;
-    thread_local std::vector<hipEvent_t> ev;
-    if (ev_dev != dev) {
-        ev.clear();   // events of another device stay allocated; a thread rarely switches
-        ev_dev = dev;
-    }
+    thread_local std::vector<hipEvent_t> by_dev[krex::kMaxDevices];
+    if (dev < 0 || dev >= krex::kMaxDevices) return nullptr;
+    std::vector<hipEvent_t> &ev = by_dev[dev];
     while (ev.size() < count) {
         hipEvent_t e = nullptr;
         if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return nullptr;
