@@ -702,14 +702,22 @@ __global__ __launch_bounds__(kThreads) void k_gen_inject(GenInjectParams Q)
         const uint64_t bfirst = P.b0 + g * G;
         const uint64_t mfirst = Q.mb0 + g * G;
         float v[4 * G];
+        words4 m[G];
+        if constexpr (DIST == NORMAL) {
+            words4 wb[G];
+            philox_blocks<G>(bfirst, P.rk, wb);
 #pragma unroll
-        for (int i = 0; i < G; ++i)
-            transform4<DIST, POW2>(philox_block(bfirst + i, P.rk), P.p0, POW2 ? P.c : P.p1, v + 4 * i);
+            for (int i = 0; i < G; ++i) transform4<DIST, POW2>(wb[i], P.p0, P.p1, v + 4 * i);
+            philox_blocks<G>(mfirst, Q.mrk, m);
+        } else {
+#pragma unroll
+            for (int i = 0; i < G; ++i)
+                transform4<DIST, POW2>(philox_block(bfirst + i, P.rk), P.p0, POW2 ? P.c : P.p1, v + 4 * i);
+#pragma unroll
+            for (int i = 0; i < G; ++i) m[i] = philox_block(mfirst + i, Q.mrk);
+        }
         pack_narrow<DT, DIST == BITCAST>(v, px.w);
         py.v = px.v;
-        words4 m[G];
-#pragma unroll
-        for (int i = 0; i < G; ++i) m[i] = philox_block(mfirst + i, Q.mrk);
         perturb_group<DT, MODE, G>(m, Q.T, Q.delta, py.s);
     };
     // offset % 4 == 0 (the launcher guarantees it), so group g's first

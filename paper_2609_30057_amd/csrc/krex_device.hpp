@@ -88,8 +88,9 @@ __device__ __forceinline__ words4 philox_block(uint64_t b, const RoundKeys &rk)
 // each round forms all 2 G products, then (behind a scheduling fence, so the
 // two phases stay apart) all 2 G xors. In a plain two-block round chain this
 // took 10% fewer cycles per block than the compiler's interleaving; in the
-// kernels it took fp8 normal generation 8% and packed fp8 normal 5% faster,
-// left the uniform generators and the packed stream's check (its two-block
+// kernels it took fp8 normal generation 8% and packed fp8 normal 5% faster
+// (generation with injection, normal: 4-6%, value and mask blocks each in
+// lockstep), left the uniform generators and the packed stream's check (its two-block
 // fp8 normal units included) unchanged, and made the check against a
 // regenerated word-stream reference 3% slower (the fence also holds back
 // the check's own work), which therefore keeps separate philox_block calls.
