@@ -776,6 +776,9 @@ def main():
                     help="fidelity modes, comma-separated from control,gated,ungated,frozen")
     ap.add_argument("--kernels", action="store_true")
     ap.add_argument("--calib-copy", action="store_true")
+    ap.add_argument("--only-gemm-large", action="store_true",
+                    help="the gemm_large command alone, without the check_stress and mixed_stream blocks "
+                         "(for profiling its kernels)")
     ap.add_argument("--configs", action="store_true")
     ap.add_argument("--cache-probe", action="store_true",
                     help="64 MiB reads warm / after a 1 GiB flush / cold, and an L2 re-read (rocprofv3 --pmc)")
@@ -812,7 +815,8 @@ def main():
             raise SystemExit("valu_rates is not built; run __graft_entry__.build()")
         sys.exit(subprocess.run([exe]).returncode)
     out = run_gemm_large(args.steps, args.warmup, not args.no_cpu_baseline)
-    out.update(run_hbm_commands())
+    if not args.only_gemm_large:
+        out.update(run_hbm_commands())
     if args.calib_copy:
         run_copy_calibration()
     if not args.no_fidelity:
