@@ -33,7 +33,10 @@
  *    reopens, and retries. The count is released when the device finishes
  *    the work (Section 5, AMD), or at once when the launch fails (Section
  *    4.2: the counter is decremented on error returns too). Without
- *    krex_attach the kernel entry points run ungated.
+ *    krex_attach the kernel entry points run ungated. A call on a stream
+ *    that is capturing into a HIP graph is recorded, not run, so it is
+ *    neither gated nor counted (nor chunked); launching the graph later is
+ *    the caller's, outside the library's count.
  *  - Chunking: with KREX_CHUNK_BYTES set (bytes, 0 or unset = off) a gated
  *    process splits krex_gen, krex_gen_packed, krex_inject, krex_gen_inject
  *    and krex_flush calls larger than that into launches of at most that
@@ -219,8 +222,11 @@ krex_status krex_check(const void *a, int32_t dta, const void *b, int32_t dtb, u
  * the array, so two calls that may overlap on one GPU (on different
  * streams, or from different threads without ordering) race and can return
  * wrong records; calls ordered on one stream are safe. When the process is
- * attached with gating, completion is tracked with a HIP event from the
- * library's event pool, as for every entry point. */
+ * attached with gating, completion is tracked, as for every entry point,
+ * with a HIP event from the pool krex_attach creates (64 per device); this
+ * call creates none: if every pooled event is in use it waits for the
+ * stream itself and then releases its count. Under graph capture it is
+ * recorded like any launch (see Gating above). */
 krex_status krex_check_noalloc(const void *a, int32_t dta, const void *b, int32_t dtb, uint64_t n, float rtol,
                                float atol, krex_check_result *out, void *stream);
 

@@ -63,11 +63,20 @@ int current_device()
 class Tracker {
 public:
     // Records a completion event for counted work on `s` and hands it to the
-    // tracking thread. On failure the count is released here.
-    krex_status track(hipStream_t s)
+    // tracking thread. On failure the count is released here. may_create =
+    // false (the entry point that allocates nothing): only a pooled event is
+    // used; with the pool empty the call waits for `s` and releases the
+    // count itself.
+    krex_status track(hipStream_t s, bool may_create = true)
     {
         const int dev = current_device();
-        hipEvent_t ev = take_event(dev);
+        hipEvent_t ev = take_event(dev, may_create);
+        if (!ev && !may_create) {
+            const hipError_t w = hipStreamSynchronize(s);
+            if (w != hipSuccess) krexg::mark_failed();
+            krexg::release(1);
+            return w == hipSuccess ? KREX_OK : hip_fail(w);
+        }
         hipError_t e = ev ? hipEventRecord(ev, s) : hipErrorOutOfMemory;
         if (e != hipSuccess) {
             if (ev) give_event(dev, ev);
@@ -99,6 +108,25 @@ public:
         return true;
     }
 
+    // Creates up to n pooled events for device dev (made current meanwhile),
+    // so that counted launches on it need not create any.
+    void prefill(int dev, size_t n)
+    {
+        if (dev < 0 || dev >= 64) return;
+        int cur = -1;
+        if (hipGetDevice(&cur) != hipSuccess) return;
+        if (cur != dev && hipSetDevice(dev) != hipSuccess) return;
+        {
+            std::lock_guard<std::mutex> g(pool_mu_);
+            while (pool_[dev].size() < n) {
+                hipEvent_t ev = nullptr;
+                if (hipEventCreateWithFlags(&ev, hipEventDisableTiming | hipEventBlockingSync) != hipSuccess) break;
+                pool_[dev].push_back(ev);
+            }
+        }
+        if (cur != dev) (void)hipSetDevice(cur);
+    }
+
     static Tracker &instance()
     {
         static Tracker *t = new Tracker();   // never destroyed; the thread is joined at exit
@@ -111,7 +139,7 @@ private:
         int dev;
     };
 
-    hipEvent_t take_event(int dev)
+    hipEvent_t take_event(int dev, bool may_create)
     {
         std::lock_guard<std::mutex> g(pool_mu_);
         if (dev >= 0 && dev < 64 && !pool_[dev].empty()) {
@@ -119,6 +147,7 @@ private:
             pool_[dev].pop_back();
             return ev;
         }
+        if (!may_create) return nullptr;
         hipEvent_t ev = nullptr;
         if (hipEventCreateWithFlags(&ev, hipEventDisableTiming | hipEventBlockingSync) != hipSuccess) return nullptr;
         return ev;
@@ -187,15 +216,27 @@ uint64_t gate_timeout_ns()
     return t;
 }
 
+// True when `s` is capturing into a HIP graph: its launches are recorded,
+// not run.
+bool capturing(hipStream_t s)
+{
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    return hipStreamIsCapturing(s, &cs) == hipSuccess && cs != hipStreamCaptureStatusNone;
+}
+
 // Counter-and-gate around one submission: admit, launch, then either track
-// its completion or release it at once on failure.
+// its completion or release it at once on failure. may_create: see
+// Tracker::track.
 template <typename F>
-krex_status submit(hipStream_t s, F &&launch_fn)
+krex_status submit(hipStream_t s, F &&launch_fn, bool may_create = true)
 {
     // With the dispatch interceptor active every kernel is counted at its
     // queue; counting here too could hold a count while the same launch
-    // waits at the gate.
-    if (krexg::intercepted()) {
+    // waits at the gate. A launch recorded into a graph runs only when the
+    // graph is launched, which this library does not see: nothing is in
+    // flight to count now, and a completion event recorded during capture
+    // would never be reached.
+    if (krexg::intercepted() || capturing(s)) {
         const hipError_t e = launch_fn();
         return e == hipSuccess ? KREX_OK : hip_fail(e);
     }
@@ -207,7 +248,7 @@ krex_status submit(hipStream_t s, F &&launch_fn)
         if (counted) krexg::release(1);
         return hip_fail(e);
     }
-    if (counted) return Tracker::instance().track(s);
+    if (counted) return Tracker::instance().track(s, may_create);
     return KREX_OK;
 }
 
@@ -262,7 +303,8 @@ template <typename F>
 krex_status submit_chunked(hipStream_t s, uint64_t n, uint64_t elem_bytes, F &&launch)
 {
     const uint64_t cb = chunk_bytes();
-    const bool chunk = cb != 0 && krexg::attached() && krexg::gated() && !krexg::intercepted() && !krexg::in_region();
+    const bool chunk = cb != 0 && krexg::attached() && krexg::gated() && !krexg::intercepted() &&
+                       !krexg::in_region() && !capturing(s);
     uint64_t per = chunk ? cb / elem_bytes : n;
     per -= per % 64;
     if (!chunk || per == 0 || n <= per) return submit(s, [&] { return launch(0, n); });
@@ -357,6 +399,11 @@ int device_cus()
 
 extern "C" {
 
+// Completion events created per device at attach, so that counted launches
+// (among them those of the entry point that allocates nothing) take pooled
+// ones.
+static constexpr size_t kEventPrefill = 64;
+
 krex_status krex_attach(int32_t device, const char *shm_name, uint32_t flags)
 {
     if (flags & ~(KREX_ATTACH_NO_GATE | KREX_ATTACH_CPU_EXCLUSIVE)) return KREX_EINVAL;
@@ -382,7 +429,10 @@ krex_status krex_attach(int32_t device, const char *shm_name, uint32_t flags)
     const uint32_t gf = ((flags & KREX_ATTACH_NO_GATE) ? krexg::kNoGate : 0u) |
                         ((flags & KREX_ATTACH_CPU_EXCLUSIVE) ? krexg::kCpuExclusive : 0u);
     const int rc = krexg::attach(name, gf);
-    if (rc == KREX_OK) g_device_attached = device;
+    if (rc == KREX_OK) {
+        g_device_attached = device;
+        if (!(flags & KREX_ATTACH_NO_GATE)) Tracker::instance().prefill(device, kEventPrefill);
+    }
     return rc;
 }
 
@@ -526,7 +576,8 @@ krex_status krex_check_noalloc(const void *a, int32_t dta, const void *b, int32_
     void *scratch = nullptr;
     const hipError_t e = krex::noalloc_scratch(&scratch);
     if (e != hipSuccess) return hip_fail(e);
-    return submit(s, [&] { return krex::launch_check(a, dta, b, dtb, n, rtol, atol, scratch, out, s); });
+    return submit(s, [&] { return krex::launch_check(a, dta, b, dtb, n, rtol, atol, scratch, out, s); },
+                  /*may_create=*/false);
 }
 
 krex_status krex_check_gen(const void *a, int32_t dta, int32_t dtb, uint64_t n, uint64_t seed, uint64_t offset,

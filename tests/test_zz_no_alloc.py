@@ -76,3 +76,81 @@ def test_size_limit_rejected_before_launch():
     assert st == -1      # KREX_EINVAL
     torch.cuda.synchronize()
     assert np.all(out.cpu().numpy() == 0xAB), "a rejected call launched nothing"
+
+
+def _attach_unique():
+    import uuid
+    shm = "/krex-na-%s" % uuid.uuid4().hex[:10]
+    krex.attach(0, shm_name=shm)
+    return shm
+
+
+def _release(shm):
+    import os
+    krex.detach()
+    try:
+        os.unlink("/dev/shm" + shm)
+    except FileNotFoundError:
+        pass
+
+
+def test_gated_calls_beyond_the_event_pool():
+    """Attached with gating, 150 calls enqueued back to back: more than the
+    64 completion events krex_attach pools, so later calls find the pool in
+    use and wait for their stream instead of creating events. Every record
+    equals krex_check's."""
+    a, b = _near_pair("f16", "f16", (1 << 20) + 5, 24)
+    ga, gb = from_storage(a, "f16"), from_storage(b, "f16")
+    shm = _attach_unique()
+    try:
+        print("no-alloc: 150 gated calls", flush=True)
+        want = krex.check(ga, gb, 1e-3, 1e-3).as_dict()
+        outs = [krex.check_result_buffer() for _ in range(150)]
+        for o in outs:
+            krex.check_noalloc(ga, gb, 1e-3, 1e-3, out=o, sync=False)
+        torch.cuda.synchronize()
+        for o in outs:
+            same_result(krex.decode_check_result(o), want)
+        assert krex.health_check() == 0
+    finally:
+        _release(shm)
+
+
+@pytest.mark.parametrize("attached", [False, True], ids=["ungated", "gated"])
+def test_graph_capture_replays(attached):
+    """The call recorded into a HIP graph (the use the entry point exists
+    for), replayed three times with eager work in between that changes the
+    reference: every replay's record equals krex_check's on the same data.
+    Attached with gating, the captured call is not counted, and the process
+    stays healthy."""
+    a, b = _near_pair("bf16", "f32", (1 << 20) + 3, 25)
+    ga, gb = from_storage(a, "bf16"), from_storage(b, "f32")
+    shm = _attach_unique() if attached else None
+    try:
+        out = krex.check_result_buffer()
+        krex.check_noalloc(ga, gb, 1.6e-2, 1e-2, out=out)    # eager first: scratch address, grid caches
+        torch.cuda.synchronize()
+        print("no-alloc: capture (attached=%s)" % attached, flush=True)
+        g = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        with torch.cuda.graph(g, stream=s, capture_error_mode="thread_local"):
+            krex.check_noalloc(ga, gb, 1.6e-2, 1e-2, out=out, sync=False)
+        torch.cuda.synchronize()
+        base = gb.clone()
+        for rep in range(3):
+            krex.inject(gb, base, 40 + rep, 0.01 * (rep + 1), 0.5, "round")   # eager: a new reference
+            torch.cuda.synchronize()
+            print("no-alloc: replay %d" % rep, flush=True)
+            g.replay()
+            torch.cuda.synchronize()
+            got = krex.decode_check_result(out)
+            same_result(got, krex.check(ga, gb, 1.6e-2, 1e-2).as_dict())
+            assert got.mismatches > 0
+        if attached:
+            assert krex.health_check() == 0
+            st = krex.gate_stats()
+            assert st["gated"]
+        del g
+    finally:
+        if attached:
+            _release(shm)
