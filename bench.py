@@ -769,6 +769,9 @@ def main():
                          "(clock, the default), or for a fixed time (time)")
     ap.add_argument("--clock-cap-ms", type=float, default=None,
                     help="fidelity: longest clock warm-up per sample (default 20 ms)")
+    ap.add_argument("--lead", type=int, default=None,
+                    help="fidelity, clock warm-up: probe launches enqueued without a wait right before each "
+                         "sample's flush and timed launch (default from the workload)")
     ap.add_argument("--sessions", type=int, default=1, help="fidelity: repeats of the compared modes")
     ap.add_argument("--dump", default=None, help="fidelity: .npz path for every sample's time and clocks")
     ap.add_argument("--durations", default=None, help="fidelity: probe durations in ms, comma-separated")
@@ -792,7 +795,7 @@ def main():
         modes = args.modes.split(",") if args.modes else None
         print(json.dumps(fidelity.run(samples=args.samples, modes=modes, siblings=args.siblings,
                                       warmup_ms=args.warmup_ms, warmup=args.warmup_mode, sessions=args.sessions,
-                                      clock_cap_ms=args.clock_cap_ms,
+                                      clock_cap_ms=args.clock_cap_ms, lead=args.lead,
                                       durations_ms=tuple(float(x) for x in args.durations.split(","))
                                       if args.durations else None, dump=args.dump)), flush=True)
         return

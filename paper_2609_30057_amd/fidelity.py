@@ -170,13 +170,13 @@ def _measure(krex, plan, samples, fl, sink, gap_ms, warmup_ms=0.0, warm_clock=No
     own region. warmup_ms > 0: warm-up launches inside the region for about
     that long before the flush and the timed launch (so the device's clocks
     settle after the siblings stop); 0: one warm-up launch. warm_clock =
-    (target_mhz, cap_ms): instead, warm-up launches one at a time, each
-    followed by a read of its clock record, until the median wave clock
-    reaches target_mhz (at least one launch; stop after cap_ms); the clock
-    that counts is the slowest wave's, since the launch lasts as long as its
-    slowest wave. Every timed
-    launch records its clocks. Returns times, drains, clock summaries and
-    warm-up launch counts per duration."""
+    (target_mhz, cap_ms, lead): instead, warm-up launches one at a time, each
+    followed by a read of its clock record, until the slowest wave's clock
+    reaches target_mhz (at least one launch; stop after cap_ms; the slowest
+    wave counts, since the launch lasts as long as it does), then `lead`
+    more launches enqueued without a wait right before the flush and the
+    timed launch. Every timed launch records its clocks. Returns times,
+    drains, clock summaries and warm-up launch counts per duration."""
     import torch
     times, drains, clocks, warms = {}, [], {}, {}
     words = krex.PROBE_WAVES * krex.PROBE_CLOCK_WORDS
@@ -192,7 +192,7 @@ def _measure(krex, plan, samples, fl, sink, gap_ms, warmup_ms=0.0, warm_clock=No
                 ts.append(krex.time_loop(fn, warm, 1, flush_buf=fl, region=True)[0])
                 nw.append(warm)
             else:
-                target, cap_ms = warm_clock
+                target, cap_ms, lead = warm_clock
                 krex.region_begin()
                 try:
                     n, t0 = 0, time.perf_counter()
@@ -202,6 +202,10 @@ def _measure(krex, plan, samples, fl, sink, gap_ms, warmup_ms=0.0, warm_clock=No
                         mhz = float(np.nanmin(krex.probe_clocks(wclk)["mhz"]))
                         if mhz >= target or (time.perf_counter() - t0) * 1e3 >= cap_ms:
                             break
+                    # lead: launches enqueued right before the flush and the
+                    # timed launch, so the device does not idle between them
+                    for _ in range(lead):
+                        krex.probe(iters, sink)
                     ts.append(krex.time_loop(fn, 0, 1, flush_buf=fl)[0])
                 finally:
                     krex.region_end()
@@ -216,7 +220,7 @@ def _measure(krex, plan, samples, fl, sink, gap_ms, warmup_ms=0.0, warm_clock=No
 
 
 def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, modes=None, warmup_ms=None,
-        settle_s=2.0, warmup=None, sessions=1, clock_cap_ms=None, dump=None):
+        settle_s=2.0, warmup=None, sessions=1, clock_cap_ms=None, dump=None, lead=None):
     """warmup: "time" (launches for about warmup_ms in each region) or
     "clock" (launches until the slowest wave's clock reaches the calibration
     median, at most clock_cap_ms), the same procedure for every mode, the
@@ -232,6 +236,7 @@ def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, mode
     warmup_ms = cfg["warmup_ms"] if warmup_ms is None else warmup_ms
     warmup = cfg["warmup"] if warmup is None else warmup
     clock_cap_ms = cfg["clock_cap_ms"] if clock_cap_ms is None else clock_cap_ms
+    lead = cfg.get("lead", 0) if lead is None else lead
     durations_ms = durations_ms or cfg["probe_ms"]
     siblings = cfg["siblings"] if siblings is None else siblings
     n = sibling_elems or W.CHECK_STRESS["rows"] * W.CHECK_STRESS["cols"]
@@ -246,7 +251,8 @@ def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, mode
               "flush_bytes": cfg["flush_bytes"], "gap_ms": cfg["gap_ms"], "P": {}, "P_median_of_10": {},
               "median_ratio": {}, "within_5pct": {}, "calibrated": {}, "sibling_GBps": {}, "drain_ms": {},
               "warmup": warmup, "warmup_ms": warmup_ms if warmup == "time" else None,
-              "clock_cap_ms": clock_cap_ms if warmup == "clock" else None, "sessions": sessions}
+              "clock_cap_ms": clock_cap_ms if warmup == "clock" else None,
+              "lead": lead if warmup == "clock" else None, "sessions": sessions}
     times, clocks, warms = {}, {}, {}
     modes = list(modes or ("native", "control", "gated", "ungated"))
     compared = [m for m in modes if m != "native"]
@@ -289,7 +295,7 @@ def run(samples=None, durations_ms=None, siblings=None, sibling_elems=None, mode
         key = (mode, sess)
         tm, drains, ck, wm = {}, [], {}, {}
         for d, iters in plan:
-            wc = (targets[d], clock_cap_ms) if warmup == "clock" else None
+            wc = (targets[d], clock_cap_ms, lead) if warmup == "clock" else None
             a, b, c, e = _measure(krex, [(d, iters)], samples, fl, sink, cfg["gap_ms"], warmup_ms, wc)
             tm.update(a)
             drains += b
