@@ -117,9 +117,11 @@ typedef struct krex_check_result {
  * highest-numbered one; KREX_REGION_CPU=none disables the pinning); region exit resumes them with SIGCONT and restores
  * the affinity before the gate reopens. A holder that dies inside such a
  * region has its stopped siblings resumed by the process that recovers the
- * lock. Returns KREX_EINVAL for unknown flags, KREX_ESTATE if already
- * attached, KREX_EPEER if the segment has another layout version,
- * KREX_ESYS on a POSIX failure. */
+ * lock. With gating it also creates 64 completion events for `device`, the
+ * pool counted launches take theirs from (more are created on demand,
+ * except by krex_check_noalloc). Returns KREX_EINVAL for unknown flags,
+ * KREX_ESTATE if already attached, KREX_EPEER if the segment has another
+ * layout version, KREX_ESYS on a POSIX failure. */
 #define KREX_ATTACH_NO_GATE 1u
 #define KREX_ATTACH_CPU_EXCLUSIVE 2u
 krex_status krex_attach(int32_t device, const char *shm_name, uint32_t flags);
