@@ -82,18 +82,22 @@ __device__ __forceinline__ words4 philox_block(uint64_t b, const RoundKeys &rk)
 }
 
 // G consecutive blocks b, b + 1, ... in lockstep, the same values as G
-// philox_block calls. On gfx950 an instruction that reads a v_mad_u64_u32
-// result right after it issues later than an independent one, and the
-// compiler's schedule places each three-way xor next to its product. Here
-// each round forms all 2 G products, then (behind a scheduling fence, so the
-// two phases stay apart) all 2 G xors. In a plain two-block round chain this
-// took 10% fewer cycles per block than the compiler's interleaving; in the
-// kernels it took fp8 normal generation 8% and packed fp8 normal 5% faster
-// (generation with injection, normal: 4-6%, value and mask blocks each in
-// lockstep), left the uniform generators and the packed stream's check (its two-block
-// fp8 normal units included) unchanged, and made the check against a
-// regenerated word-stream reference 3% slower (the fence also holds back
-// the check's own work), which therefore keeps separate philox_block calls.
+// philox_block calls. On gfx950 a run of v_mad_u64_u32 products issues
+// faster than products interleaved one by one with other vector
+// instructions (eight products, then eight xors: 8.3-8.4 cycles per pair;
+// alternating: 9.5, whether or not the xor reads the product and whatever
+// the register banks), and the compiler's schedule places each three-way
+// xor next to its product. Here each round forms all 2 G products, then
+// (behind a scheduling fence, so the two phases stay apart) all 2 G xors.
+// In a plain two-block round chain this took 10% fewer cycles per block
+// than the compiler's interleaving; in the kernels it took fp8 normal
+// generation 8% and packed fp8 normal 5% faster (generation with
+// injection, normal: 4-6%, value and mask blocks each in lockstep), left
+// the uniform generators (also with two units' blocks in one lockstep) and
+// the packed stream's check (its two-block fp8 normal units included)
+// unchanged, and made the check against a regenerated word-stream
+// reference 3% slower (the fence also holds back the check's own work),
+// which therefore keeps separate philox_block calls.
 template <int G>
 __device__ __forceinline__ void philox_blocks(uint64_t b, const RoundKeys &rk, words4 (&o)[G])
 {
