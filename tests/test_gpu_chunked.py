@@ -74,3 +74,54 @@ def test_chunked_submissions_write_the_same_values():
     except FileNotFoundError:
         pass
     assert r.returncode == 0 and "chunked ok" in r.stdout, (r.returncode, r.stdout[-2000:], r.stderr[-4000:])
+
+
+CAPTURE_CHILD = r'''
+import sys
+sys.path.insert(0, sys.argv[1])
+import torch
+import oracle
+import paper_2609_30057_amd as krex
+from tests.gpu_helpers import assert_bits_equal, empty, to_storage
+
+torch.cuda.set_device(0)
+krex.attach(0, shm_name=sys.argv[2])
+n = (3 << 20) + 77
+x = empty("f16", n)
+krex.gen(x, 2, 4, "uniform", -4.0, 4.0)          # eager first
+torch.cuda.synchronize()
+print("chunked capture: record", flush=True)
+g = torch.cuda.CUDAGraph()
+s = torch.cuda.Stream()
+with torch.cuda.graph(g, stream=s, capture_error_mode="thread_local"):
+    krex.gen(x, 2, 4, "uniform", -4.0, 4.0)
+torch.cuda.synchronize()
+xr = oracle.gen("f16", n, 2, 4, 0, -4.0, 4.0)
+for rep in range(3):
+    x.zero_()
+    torch.cuda.synchronize()
+    print("chunked capture: replay %d" % rep, flush=True)
+    g.replay()
+    torch.cuda.synchronize()
+    assert_bits_equal(to_storage(x, "f16"), xr, "captured gen")
+assert krex.health_check() == 0
+del g
+krex.detach()
+print("capture ok", flush=True)
+'''
+
+
+def test_capture_is_not_chunked():
+    """A gated process with chunking on records a large generation into a
+    HIP graph: under capture the call is neither chunked nor counted (its
+    launches only run when the graph does), and every replay writes the
+    oracle's values."""
+    shm = "/krex-chunkcap-%s" % uuid.uuid4().hex[:10]
+    env = dict(os.environ, KREX_CHUNK_BYTES=str(1 << 20), KREX_CHUNK_DEPTH="2")
+    r = subprocess.run([sys.executable, "-c", CAPTURE_CHILD, ROOT, shm], env=env, capture_output=True, text=True,
+                       timeout=300)
+    try:
+        os.unlink("/dev/shm" + shm)
+    except FileNotFoundError:
+        pass
+    assert r.returncode == 0 and "capture ok" in r.stdout, (r.returncode, r.stdout[-2000:], r.stderr[-4000:])
